@@ -1,0 +1,319 @@
+"""Benchmark of one decode step of paged decode attention on one MI355X.
+
+A step is one pass of the whole hot path over one batch: the split-KV decode
+kernel followed by the cross-split reduce, for every sequence and head of the
+batch.  The default workload is the SQL-generator stage (batch 64, 32 query /
+8 KV heads, head_dim 128, a 2048-token schema prefix shared by every
+sequence plus a unique 64..512-token suffix, 16-token blocks, 512-token
+partitions), with seeded synthetic bf16 N(0,1) inputs.
+
+Timing: the pools and queries are replicated R times in HBM (R copies of the
+same data at different addresses, like R layers of a model) and consecutive
+steps rotate through them, so a step does not find its working set in the
+256 MB Infinity Cache left over from the previous step.  W warmup steps,
+then K timed steps bracketed by device synchronisation; per-kernel durations
+come from HIP events recorded around every launch on the launch stream.
+
+Output: exactly one JSON line on stdout.  `value` is KV GB/s counting the
+algorithmic bytes of a step (each distinct cached token slot once, plus
+queries, outputs, block tables and lengths) over the measured step time.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1..5]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = ["paper_2510_14126_amd/csrc/decode_valu.hip", "paper_2510_14126_amd/csrc/pa_device.h"]
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def byte_accounting(w):
+    from workloads import logical_tokens, touched_slots
+    per_tok = w.bytes_per_token
+    qo = 2 * (w.batch * w.num_q_heads * w.head_dim * 2)               # q in + out
+    meta = 4 * w.batch + 4 * int(w.blocks_per_seq().sum())              # lengths + table entries read
+    alg = touched_slots(w) * per_tok + qo + meta
+    logical = logical_tokens(w) * per_tok + qo + meta
+    return alg, logical
+
+
+# --------------------------------------------------------------- CPU baseline
+
+_W = None
+
+
+def _oracle_chunk(seqs):
+    from threadpoolctl import threadpool_limits
+    from oracle import decode_workload
+    with threadpool_limits(1):
+        decode_workload(_W, seqs=seqs)
+    return len(seqs)
+
+
+def cpu_baseline(w, alg_bytes, min_seconds=10.0):
+    """Time the CPU oracle on whole decode steps of the same batch.
+
+    The oracle runs over the batch's sequences in a process pool (one BLAS
+    thread per worker) and the step is repeated until min_seconds pass.
+    """
+    import multiprocessing as mp
+    global _W
+    _W = w
+    cores = max(1, min(16, len(os.sched_getaffinity(0))))
+    chunks = [list(range(i, w.batch, cores)) for i in range(cores)]
+    chunks = [c for c in chunks if c]
+    ctx = mp.get_context("fork")
+    steps = 0
+    with ctx.Pool(len(chunks)) as pool:
+        pool.map(_oracle_chunk, [chunks[0][:1]])                   # workers up
+        t0 = time.perf_counter()
+        while True:
+            pool.map(_oracle_chunk, chunks)
+            steps += 1
+            el = time.perf_counter() - t0
+            if el >= min_seconds:
+                break
+    sec_per_step = el / steps
+    return {"value": round(alg_bytes / sec_per_step / 1e9, 4), "unit": "GB/s", "cores": len(chunks),
+            "kind": "oracle", "sample": f"{steps} full decode steps of the same batch "
+            f"({w.batch} sequences) in {el:.1f} s; fp64 numpy oracle, process pool, "
+            f"1 BLAS thread per worker", "seconds_per_step": round(sec_per_step, 4),
+            "decode_steps_per_s": round(1.0 / sec_per_step, 3)}
+
+
+# ------------------------------------------------------------------ traffic
+
+def traffic_from_profiles(workload_name):
+    """Counter-derived HBM bytes per decode launch, if the profile summary was
+    taken on the current kernel source; else None."""
+    path = os.path.join(PROFILE_DIR, f"decode_valu_{workload_name}_counters.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_src = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    m_tr = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_src or not m_tr or m_src.group(1) != kernel_source_hash():
+        return None
+    return float(m_tr.group(1))
+
+
+# ---------------------------------------------------------------- GPU timing
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--partition-size", type=int, default=None)
+    ap.add_argument("--replicas", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--profile-loop", type=int, default=0,
+                    help="only run this many decode launches (plus one calibration copy) and exit; "
+                         "for hardware-counter runs")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE={world}); "
+              "the hot path is not distributed in this build", file=sys.stderr)
+        sys.exit(2)
+
+    from workloads import build_config
+    t0 = time.perf_counter()
+    w = build_config(args.config)
+    if args.partition_size is not None:
+        w.partition_size = args.partition_size
+    alg_bytes, logical_bytes = byte_accounting(w)
+    log(f"workload {w.name}: B={w.batch} Hq={w.num_q_heads} Hkv={w.num_kv_heads} D={w.head_dim} "
+        f"NB={w.num_blocks} max_ctx={w.max_context_len} alg={alg_bytes/1e6:.1f} MB "
+        f"logical={logical_bytes/1e6:.1f} MB (built in {time.perf_counter()-t0:.1f} s)")
+
+    cpu = None
+    if not args.no_cpu_baseline and not args.profile_loop:
+        log("cpu baseline (oracle) ...")
+        cpu = cpu_baseline(w, alg_bytes, args.cpu_seconds)
+        log(f"cpu baseline: {cpu}")
+
+    import torch
+    from paper_2510_14126_amd import binding
+    from paper_2510_14126_amd.device import PagedBatch
+
+    dev = torch.device("cuda:0")
+    pool_bytes = 2 * w.k_pool.nbytes
+    R = args.replicas or max(1, min(16, -(-(1 << 30) // pool_bytes)))
+    base = PagedBatch(w, dev)
+    reps = [(base.pool, base.q)]
+    keep = []
+    for _ in range(1, R):
+        k, v, q = base.k.clone(), base.v.clone(), base.q.clone()
+        keep.append((k, v, q))
+        reps.append((binding.kv_pool_create(w.num_blocks, 16, w.num_kv_heads, w.head_dim, k, v), q))
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    split = base.num_parts > 1
+
+    def decode(i):
+        pool, q = reps[i % R]
+        binding.paged_attn_decode(pool, q, base.bt, base.bt_stride, base.ctx, base.batch, base.hq,
+                                  w.scale, base.max_ctx, base.partition_size, base.out,
+                                  base.part_o, base.part_lse, sh)
+
+    def reduce():
+        binding.paged_attn_reduce(base.part_o, base.part_lse, base.ctx, base.batch, base.hq,
+                                  base.d, base.partition_size, base.num_parts, base.out, sh)
+
+    if args.profile_loop:
+        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        binding.pa_stream_copy(src, dst, src.numel(), sh)      # calibration: 256 MiB each way
+        for i in range(args.profile_loop):
+            decode(i)
+            if split:
+                reduce()
+        torch.cuda.synchronize()
+        log(f"profile loop done: {args.profile_loop} decode launches, replicas={R}, "
+            f"calibration copy 268435456 bytes")
+        return
+
+    for i in range(args.warmup):
+        decode(i)
+        if split:
+            reduce()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(K):
+        e = ev[i]
+        e[0].record(stream)
+        decode(i)
+        e[1].record(stream)
+        if split:
+            reduce()
+        e[2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    dec_ms = np.array([ev[i][0].elapsed_time(ev[i][1]) for i in range(K)])
+    red_ms = np.array([ev[i][1].elapsed_time(ev[i][2]) for i in range(K)])
+    span_ms = ev[0][0].elapsed_time(ev[K - 1][2])
+    ms_step = span_ms / K
+
+    # hot: one replica, same loop
+    hot = []
+    for i in range(K):
+        e0 = torch.cuda.Event(enable_timing=True); e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        pool, q = reps[0]
+        binding.paged_attn_decode(pool, q, base.bt, base.bt_stride, base.ctx, base.batch, base.hq,
+                                  w.scale, base.max_ctx, base.partition_size, base.out,
+                                  base.part_o, base.part_lse, sh)
+        if split:
+            reduce()
+        e1.record(stream)
+        hot.append((e0, e1))
+    torch.cuda.synchronize()
+    hot_ms = float(np.mean([a.elapsed_time(b) for a, b in hot]))
+
+    # achievable copy bandwidth on this machine (read + write bytes)
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        binding.pa_stream_copy(src, dst, src.numel(), sh)
+    c0 = torch.cuda.Event(enable_timing=True); c1 = torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    for _ in range(10):
+        binding.pa_stream_copy(src, dst, src.numel(), sh)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbps = 10 * 2 * src.numel() / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del src, dst
+
+    # parity spot check of the benchmarked launch configuration
+    from oracle import compare, decode_workload
+    torch.cuda.synchronize()
+    base.out.zero_()
+    decode(0)
+    if split:
+        reduce()
+    torch.cuda.synchronize()
+    seqs = [0, int(np.argmax(w.context_lens)), w.batch - 1]
+    ref, _ = decode_workload(w, seqs=seqs)
+    rep = compare(base.out_bits()[seqs], ref)
+    log(f"parity spot check on sequences {seqs}: {rep}")
+
+    dec_avg = float(dec_ms.mean())
+    achieved = alg_bytes / (dec_avg * 1e-3) / 1e9
+    value = alg_bytes / (ms_step * 1e-3) / 1e9
+    traffic = traffic_from_profiles(w.name)
+    line = {
+        "metric": "paged decode-attention KV GB/s (algorithmic bytes) and % of HBM peak; "
+                  "decode steps/s per batch",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 K/V/Q; stage-shaped block tables and lengths)",
+        "config": {"workload": f"{w.name}: {w.meta['description']}", "batch": w.batch,
+                   "num_q_heads": w.num_q_heads, "num_kv_heads": w.num_kv_heads,
+                   "head_dim": w.head_dim, "block_size": 16, "partition_size": base.partition_size,
+                   "num_partitions": base.num_parts, "replicas_rotated": R,
+                   "max_context_len": w.max_context_len, "parallelism": "single GPU"},
+        "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
+        "decode_steps_per_s": round(1000.0 / ms_step, 2),
+        "tokens_per_s": round(w.batch * 1000.0 / ms_step, 1),
+        "algorithmic_bytes_per_step": int(alg_bytes),
+        "logical_kv_gbps_effective": round(logical_bytes / (ms_step * 1e-3) / 1e9, 2),
+        "hot_ms_per_step": round(hot_ms, 5),
+        "kernel_ms": {"decode_avg": round(dec_avg, 5), "reduce_avg": round(float(red_ms.mean()), 5)},
+        "copy_probe_gbps": round(copy_gbps, 1),
+        "pct_of_copy_probe": round(100 * value / copy_gbps, 2),
+        "wall_s_timed_region": round(wall, 4),
+        "parity_spot_check": {"passed": rep.passed, "max_abs": rep.max_abs,
+                              "worst_row_rel_l2": rep.worst_row_rel_l2},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic, "kernel": "decode_valu_kernel<128,4>",
+                     "bytes_per_launch": int(alg_bytes)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

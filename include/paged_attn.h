@@ -1,0 +1,212 @@
+/*
+ * paged_attn.h -- C ABI of the MI355X (gfx950) paged decode-attention library.
+ *
+ * The operation.  An LLM stage of an agentic workflow keeps the prompt
+ * context of its calls resident in GPU memory, so successive calls of the
+ * stage -- the retries of an SQL error fixer against one schema, the
+ * generator calls that all start from that schema -- reuse it instead of
+ * rebuilding it (Cortex paper, section 1 "Motivating Example" and section 2
+ * "Cortex Benefits", Fig. 2).  That resident context is a paged KV cache: a
+ * pool of fixed-size token blocks, reached per sequence through a block
+ * table, where shared prompt blocks appear in many tables.  Each decode step
+ * of the stage runs, per layer, scaled dot-product softmax attention of one
+ * new query row per head over the sequence's whole cached context:
+ *
+ *     out[b][h] = sum_t softmax_t(scale * <q[b][h], K_g[t]>) V_g[t],
+ *     g = h / (Hq / Hkv),  t = 0 .. ctx[b]-1,
+ *
+ * where token t of sequence b is row t % 16 of physical block
+ * block_tables[b][t / 16].  The paper gives no kernel or formula; this is the
+ * textbook definition, which the library reaches through an online softmax,
+ * optional split-KV partitions and a log-sum-exp merge.
+ *
+ * Data types and layouts (all row-major, little-endian):
+ *   bf16    16-bit brain float, stored as uint16 bit patterns.
+ *   K pool  bf16 [num_blocks][num_kv_heads][16][head_dim]   (token-major tiles)
+ *   V pool  same shape and layout as the K pool.
+ *   q       bf16 [batch][num_q_heads][head_dim]
+ *   out     bf16 [batch][num_q_heads][head_dim], rounded to nearest even from
+ *           fp32 accumulation.
+ *   partial_out  fp32 [batch][num_q_heads][max_partitions][head_dim]
+ *   partial_lse  fp32 [batch][num_q_heads][max_partitions]
+ *
+ * Ownership.  The caller owns every device buffer (pools, q, tables,
+ * lengths, outputs, partials).  The library never allocates device memory
+ * and never creates streams; a pool handle owns host-side metadata only.
+ * Handles are not thread-safe: callers serialise access to one handle.
+ *
+ * Errors.  Every function returns 0 (PA_OK) or a negative PA_E* code and
+ * never aborts; pa_last_error() returns a thread-local description of the
+ * last failure.  Host-visible arguments are validated before any HIP call.
+ * Device-resident data (table entries, context lengths) is not validated,
+ * but kernels stay memory-safe: ids are clamped into [0, num_blocks) and
+ * lengths into [0, max_context_len], so bad data gives unspecified values,
+ * never an out-of-bounds access.
+ *
+ * Streams.  `stream` is a hipStream_t passed as void* (NULL = the default
+ * stream).  Kernels are enqueued asynchronously; a function returning PA_OK
+ * only means the launch was accepted.
+ */
+#ifndef PAGED_ATTN_H
+#define PAGED_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  PA_OK = 0,
+  PA_EINVAL = -1,       /* bad argument: null, misaligned, out of range, inconsistent */
+  PA_ENOMEM = -2,       /* the block pool has too few free blocks */
+  PA_EUNSUPPORTED = -3, /* valid but unsupported geometry (head_dim, group size) */
+  PA_EHIP = -4,         /* a HIP runtime call failed (message says which) */
+  PA_ESTATE = -5        /* allocator state violation: double release, claim of a used block */
+};
+
+#define PA_BLOCK_SIZE 16
+
+typedef struct pa_kv_pool pa_kv_pool;
+
+/* Thread-local description of the last error (never NULL). */
+const char *pa_last_error(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int32_t pa_version(void);
+
+/* ---------------------------------------------------------------------------
+ * KV block pool: layout plus a host-side allocator with reference counts.
+ *
+ * One pool per stage engine (paper section 2: "a dedicated engine pool for
+ * every workflow stage", each with "its own queue, cache").  A block that
+ * holds shared prompt tokens is retained once per extra sequence that maps
+ * it and returns to the free list when its count reaches zero.
+ * ------------------------------------------------------------------------- */
+
+/* Create a pool handle over caller-owned device buffers.
+ *   num_blocks    > 0 physical blocks in each of the K and V pools
+ *   block_size    must be 16 (tokens per block)
+ *   num_kv_heads  1 .. 64
+ *   head_dim      64 or 128 (others: PA_EUNSUPPORTED)
+ *   k_pool,v_pool device pointers, 256-byte aligned, each holding
+ *                 num_blocks*num_kv_heads*16*head_dim bf16 values
+ *   out           receives the handle; *out is untouched on error.
+ * All blocks start free. */
+int kv_pool_create(int32_t num_blocks, int32_t block_size, int32_t num_kv_heads,
+                   int32_t head_dim, void *k_pool, void *v_pool, pa_kv_pool **out);
+
+/* Destroy a handle (the device buffers stay the caller's).  NULL is a no-op. */
+int kv_pool_destroy(pa_kv_pool *pool);
+
+/* Take n free blocks (all or nothing), each with reference count 1, and
+ * write their ids to ids_out[0..n-1].  PA_ENOMEM if fewer than n are free. */
+int kv_pool_alloc(pa_kv_pool *pool, int32_t n, int32_t *ids_out);
+
+/* Take the n listed blocks (all or nothing), each with reference count 1.
+ * PA_ESTATE if any is in use or listed twice; PA_EINVAL if out of range.
+ * Used when a caller has already chosen the physical placement. */
+int kv_pool_claim(pa_kv_pool *pool, int32_t n, const int32_t *ids);
+
+/* Add one reference to each listed block (sharing a prefix with one more
+ * sequence).  PA_ESTATE if any listed block is free; nothing changes then. */
+int kv_pool_retain(pa_kv_pool *pool, int32_t n, const int32_t *ids);
+
+/* Drop one reference per listing; a block whose count reaches 0 is freed.
+ * PA_ESTATE (and nothing changes) if any block would drop below zero. */
+int kv_pool_release(pa_kv_pool *pool, int32_t n, const int32_t *ids);
+
+/* Number of free blocks. */
+int kv_pool_num_free(const pa_kv_pool *pool, int32_t *n_out);
+
+/* Reference count of one block (0 = free). */
+int kv_pool_refcount(const pa_kv_pool *pool, int32_t id, int32_t *count_out);
+
+/* Geometry: element strides of the pool [block][kv_head][token][dim], and
+ * the bytes of one pool (K or V). */
+int kv_pool_layout(const pa_kv_pool *pool, int64_t elem_strides_out[4], int64_t *pool_bytes_out);
+
+/* ---------------------------------------------------------------------------
+ * Decode attention.
+ * ------------------------------------------------------------------------- */
+
+/* Number of split-KV partitions for a batch whose longest context is
+ * max_context_len: ceil(max_context_len / partition_size), at least 1;
+ * partition_size 0 means one pass over the whole context (1 partition). */
+int paged_attn_num_partitions(int32_t max_context_len, int32_t partition_size, int32_t *p_out);
+
+/* Bytes of partial_out and partial_lse that paged_attn_decode needs when it
+ * splits (num_partitions > 1); both are 0 when it does not. */
+int paged_attn_workspace_size(int32_t batch, int32_t num_q_heads, int32_t head_dim,
+                              int32_t max_context_len, int32_t partition_size,
+                              size_t *partial_out_bytes, size_t *partial_lse_bytes);
+
+/* One decode step of attention for a batch over a paged KV pool.
+ *   pool             geometry and K/V device pointers (kv_pool_create)
+ *   q                device bf16 [batch][num_q_heads][head_dim], 16-byte aligned
+ *   block_tables     device int32 [batch][bt_stride]; entries 0..ceil(ctx/16)-1
+ *                    of row b are physical ids, later entries are never read
+ *   bt_stride        >= ceil(max_context_len / 16)
+ *   context_lens     device int32 [batch]: tokens to attend (the current token
+ *                    included); 0 gives a zero output row
+ *   batch            >= 0 (0 is a no-op)
+ *   num_q_heads      multiple of the pool's num_kv_heads; the group size
+ *                    G = num_q_heads / num_kv_heads must be 4 or 8
+ *   scale            softmax scale applied to the fp32 dot products
+ *   max_context_len  host upper bound of context_lens; sizes the grid
+ *   partition_size   split-KV partition in tokens, a multiple of 16; 0 = none
+ *   out              device bf16 [batch][num_q_heads][head_dim]; written when
+ *                    there is a single partition
+ *   partial_out/_lse device fp32 partials (paged_attn_workspace_size), required
+ *                    when there is more than one partition; the caller then
+ *                    runs paged_attn_reduce on the same stream
+ * G = 4 runs on VALU dot products, G = 8 on MFMA tiles. */
+int paged_attn_decode(const pa_kv_pool *pool, const void *q, const int32_t *block_tables,
+                      int32_t bt_stride, const int32_t *context_lens, int32_t batch,
+                      int32_t num_q_heads, float scale, int32_t max_context_len,
+                      int32_t partition_size, void *out, float *partial_out,
+                      float *partial_lse, void *stream);
+
+/* Merge split-KV partials into the bf16 output: for each (b, h) with
+ * P_b = ceil(ctx_b / partition_size) partitions, weights w_p = exp(lse_p - max
+ * lse) and out = sum_p w_p o_p / sum_p w_p; P_b = 0 gives zeros.  A sequence
+ * with one partition reproduces the single-pass output bit for bit.
+ *   max_partitions   the P dimension of the partial buffers (>= every P_b)
+ * Other arguments as in paged_attn_decode. */
+int paged_attn_reduce(const float *partial_out, const float *partial_lse,
+                      const int32_t *context_lens, int32_t batch, int32_t num_q_heads,
+                      int32_t head_dim, int32_t partition_size, int32_t max_partitions,
+                      void *out, void *stream);
+
+/* Index-trace variant of paged_attn_decode, for verifying block-table and
+ * context-length handling.  It runs the same gather code and, in addition,
+ * records for every work item (partition p, sequence b, KV head g) the
+ * ordered list of KV tiles it loaded as int32 triples (logical block j,
+ * physical id as read from the table, valid rows):
+ *   trace[((p * batch + b) * num_kv_heads + g) * trace_tiles + i][3]
+ * for the i-th tile, trace_tiles = partition_size / 16 (or
+ * ceil(max_context_len / 16) without partitions).  Entries past the last
+ * tile are left untouched.  trace_capacity is the number of int32 values
+ * the buffer holds; PA_EINVAL if it is too small. */
+int paged_attn_decode_trace(const pa_kv_pool *pool, const void *q, const int32_t *block_tables,
+                            int32_t bt_stride, const int32_t *context_lens, int32_t batch,
+                            int32_t num_q_heads, float scale, int32_t max_context_len,
+                            int32_t partition_size, void *out, float *partial_out,
+                            float *partial_lse, int32_t *trace, int64_t trace_capacity,
+                            void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Measurement helper.
+ * ------------------------------------------------------------------------- */
+
+/* Plain device-to-device copy of `bytes` (a multiple of 16; both pointers
+ * 16-byte aligned) with a streaming kernel; used to calibrate hardware
+ * traffic counters and the achievable HBM bandwidth. */
+int pa_stream_copy(const void *src, void *dst, size_t bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PAGED_ATTN_H */

@@ -1,0 +1,372 @@
+// C ABI of the paged decode-attention library: KV block pool allocator,
+// argument validation and launch planning.  Every check runs on the host
+// before any HIP call, so all validation paths work without a GPU.
+#include "../../include/paged_attn.h"
+#include "kernels.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+struct pa_kv_pool {
+  int32_t num_blocks;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  const uint16_t* k;
+  const uint16_t* v;
+  std::vector<int32_t> refcount;  // 0 = free
+  std::vector<int32_t> free_stack; // top = back(); ids pop in ascending order initially
+};
+
+namespace {
+
+thread_local std::string g_err = "no error";
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Rebuild the free stack from refcounts (ascending ids pop first).
+void rebuild_free(pa_kv_pool* pool) {
+  pool->free_stack.clear();
+  for (int32_t id = pool->num_blocks - 1; id >= 0; --id)
+    if (pool->refcount[id] == 0) pool->free_stack.push_back(id);
+}
+
+int check_ids(const pa_kv_pool* pool, int32_t n, const int32_t* ids, const char* fn) {
+  if (!pool) return fail(PA_EINVAL, "%s: pool is NULL", fn);
+  if (n < 0) return fail(PA_EINVAL, "%s: n = %d < 0", fn, n);
+  if (n > 0 && !ids) return fail(PA_EINVAL, "%s: ids is NULL", fn);
+  for (int32_t i = 0; i < n; ++i)
+    if (ids[i] < 0 || ids[i] >= pool->num_blocks)
+      return fail(PA_EINVAL, "%s: id %d at position %d outside [0, %d)", fn, ids[i], i,
+                  pool->num_blocks);
+  return PA_OK;
+}
+
+struct Plan {
+  int32_t group;
+  int32_t part_tokens;
+  int32_t num_parts;
+};
+
+int plan(int32_t max_context_len, int32_t partition_size, Plan* out, const char* fn) {
+  if (max_context_len < 0) return fail(PA_EINVAL, "%s: max_context_len = %d < 0", fn, max_context_len);
+  if (partition_size < 0 || partition_size % PA_BLOCK_SIZE != 0)
+    return fail(PA_EINVAL, "%s: partition_size = %d is not a non-negative multiple of %d", fn,
+                partition_size, PA_BLOCK_SIZE);
+  const int64_t whole = ((int64_t)max_context_len + PA_BLOCK_SIZE - 1) / PA_BLOCK_SIZE * PA_BLOCK_SIZE;
+  if (partition_size == 0 || whole <= partition_size) {
+    out->part_tokens = (int32_t)(whole > 0 ? whole : PA_BLOCK_SIZE);
+    out->num_parts = 1;
+  } else {
+    out->part_tokens = partition_size;
+    out->num_parts = (int32_t)(((int64_t)max_context_len + partition_size - 1) / partition_size);
+  }
+  return PA_OK;
+}
+
+int decode_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tables,
+                int32_t bt_stride, const int32_t* context_lens, int32_t batch,
+                int32_t num_q_heads, float scale, int32_t max_context_len, int32_t partition_size,
+                void* out, float* partial_out, float* partial_lse, int32_t* trace,
+                int64_t trace_capacity, bool tracing, void* stream, const char* fn) {
+  if (!pool) return fail(PA_EINVAL, "%s: pool is NULL", fn);
+  if (batch < 0) return fail(PA_EINVAL, "%s: batch = %d < 0", fn, batch);
+  if (num_q_heads <= 0 || num_q_heads % pool->num_kv_heads != 0)
+    return fail(PA_EINVAL, "%s: num_q_heads = %d is not a positive multiple of num_kv_heads = %d",
+                fn, num_q_heads, pool->num_kv_heads);
+  const int32_t group = num_q_heads / pool->num_kv_heads;
+  if (group != 4 && group != 8)
+    return fail(PA_EUNSUPPORTED, "%s: query heads per KV head = %d (supported: 4, 8)", fn, group);
+  if (!(scale == scale) || scale == __builtin_inff() || scale == -__builtin_inff())
+    return fail(PA_EINVAL, "%s: scale is not finite", fn);
+  Plan pl;
+  int rc = plan(max_context_len, partition_size, &pl, fn);
+  if (rc) return rc;
+  const int64_t need_bt = ((int64_t)max_context_len + PA_BLOCK_SIZE - 1) / PA_BLOCK_SIZE;
+  if (bt_stride < need_bt || bt_stride < 0)
+    return fail(PA_EINVAL, "%s: bt_stride = %d < ceil(max_context_len / 16) = %lld", fn, bt_stride,
+                (long long)need_bt);
+  const int64_t grid = (int64_t)pl.num_parts * batch * pool->num_kv_heads;
+  if (grid > 0x7fffffffLL) return fail(PA_EINVAL, "%s: grid of %lld workgroups is too large", fn, (long long)grid);
+  if (batch == 0) return PA_OK;
+  if (!q || !block_tables || !context_lens)
+    return fail(PA_EINVAL, "%s: q, block_tables and context_lens must be non-NULL", fn);
+  if (!aligned(q, 16)) return fail(PA_EINVAL, "%s: q is not 16-byte aligned", fn);
+  if (!aligned(block_tables, 4) || !aligned(context_lens, 4))
+    return fail(PA_EINVAL, "%s: block_tables/context_lens are not 4-byte aligned", fn);
+  const bool split = pl.num_parts > 1;
+  if (!split) {
+    if (!out) return fail(PA_EINVAL, "%s: out is NULL (single partition)", fn);
+    if (!aligned(out, 4)) return fail(PA_EINVAL, "%s: out is not 4-byte aligned", fn);
+  } else {
+    if (!partial_out || !partial_lse)
+      return fail(PA_EINVAL, "%s: %d partitions need partial_out and partial_lse", fn, pl.num_parts);
+    if (!aligned(partial_out, 16) || !aligned(partial_lse, 4))
+      return fail(PA_EINVAL, "%s: partial buffers are misaligned", fn);
+  }
+  const int32_t trace_tiles = pl.part_tokens / PA_BLOCK_SIZE;
+  if (tracing) {
+    const int64_t need = grid * trace_tiles * 3;
+    if (!trace || !aligned(trace, 4)) return fail(PA_EINVAL, "%s: trace buffer is NULL or misaligned", fn);
+    if (trace_capacity < need)
+      return fail(PA_EINVAL, "%s: trace_capacity %lld < %lld int32 values", fn,
+                  (long long)trace_capacity, (long long)need);
+  }
+
+  pa::DecodeParams p{};
+  p.k_pool = pool->k;
+  p.v_pool = pool->v;
+  p.q = static_cast<const uint16_t*>(q);
+  p.block_tables = block_tables;
+  p.context_lens = context_lens;
+  p.out = static_cast<uint16_t*>(out);
+  p.part_o = partial_out;
+  p.part_lse = partial_lse;
+  p.trace = trace;
+  p.num_blocks = pool->num_blocks;
+  p.num_kv_heads = pool->num_kv_heads;
+  p.num_q_heads = num_q_heads;
+  p.batch = batch;
+  p.bt_stride = bt_stride;
+  p.max_ctx = max_context_len;
+  p.part_tokens = pl.part_tokens;
+  p.num_parts = pl.num_parts;
+  p.trace_tiles = trace_tiles;
+  p.scale_log2 = scale * 1.4426950408889634f;
+  hipError_t e = pa::launch_decode_valu(p, pool->head_dim, group, tracing,
+                                        static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
+  return PA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pa_last_error(void) { return g_err.c_str(); }
+
+int32_t pa_version(void) { return 100; }
+
+int kv_pool_create(int32_t num_blocks, int32_t block_size, int32_t num_kv_heads, int32_t head_dim,
+                   void* k_pool, void* v_pool, pa_kv_pool** out) {
+  if (!out) return fail(PA_EINVAL, "kv_pool_create: out is NULL");
+  if (num_blocks <= 0) return fail(PA_EINVAL, "kv_pool_create: num_blocks = %d <= 0", num_blocks);
+  if (block_size != PA_BLOCK_SIZE)
+    return fail(PA_EINVAL, "kv_pool_create: block_size = %d (must be %d)", block_size, PA_BLOCK_SIZE);
+  if (num_kv_heads < 1 || num_kv_heads > 64)
+    return fail(PA_EINVAL, "kv_pool_create: num_kv_heads = %d outside [1, 64]", num_kv_heads);
+  if (head_dim != 64 && head_dim != 128)
+    return fail(PA_EUNSUPPORTED, "kv_pool_create: head_dim = %d (supported: 64, 128)", head_dim);
+  if (!k_pool || !v_pool) return fail(PA_EINVAL, "kv_pool_create: pool pointers must be non-NULL");
+  if (!aligned(k_pool, 16) || !aligned(v_pool, 16))
+    return fail(PA_EINVAL, "kv_pool_create: pool pointers must be 16-byte aligned");
+  pa_kv_pool* p = new (std::nothrow) pa_kv_pool;
+  if (!p) return fail(PA_ENOMEM, "kv_pool_create: host allocation failed");
+  p->num_blocks = num_blocks;
+  p->num_kv_heads = num_kv_heads;
+  p->head_dim = head_dim;
+  p->k = static_cast<const uint16_t*>(k_pool);
+  p->v = static_cast<const uint16_t*>(v_pool);
+  p->refcount.assign(num_blocks, 0);
+  rebuild_free(p);
+  *out = p;
+  return PA_OK;
+}
+
+int kv_pool_destroy(pa_kv_pool* pool) {
+  delete pool;
+  return PA_OK;
+}
+
+int kv_pool_alloc(pa_kv_pool* pool, int32_t n, int32_t* ids_out) {
+  if (!pool) return fail(PA_EINVAL, "kv_pool_alloc: pool is NULL");
+  if (n < 0) return fail(PA_EINVAL, "kv_pool_alloc: n = %d < 0", n);
+  if (n > 0 && !ids_out) return fail(PA_EINVAL, "kv_pool_alloc: ids_out is NULL");
+  if ((size_t)n > pool->free_stack.size())
+    return fail(PA_ENOMEM, "kv_pool_alloc: %d blocks requested, %zu free", n, pool->free_stack.size());
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t id = pool->free_stack.back();
+    pool->free_stack.pop_back();
+    pool->refcount[id] = 1;
+    ids_out[i] = id;
+  }
+  return PA_OK;
+}
+
+int kv_pool_claim(pa_kv_pool* pool, int32_t n, const int32_t* ids) {
+  int rc = check_ids(pool, n, ids, "kv_pool_claim");
+  if (rc) return rc;
+  std::vector<char> seen(pool->num_blocks, 0);
+  for (int32_t i = 0; i < n; ++i) {
+    if (pool->refcount[ids[i]] != 0)
+      return fail(PA_ESTATE, "kv_pool_claim: block %d is already in use", ids[i]);
+    if (seen[ids[i]]) return fail(PA_ESTATE, "kv_pool_claim: block %d listed twice", ids[i]);
+    seen[ids[i]] = 1;
+  }
+  for (int32_t i = 0; i < n; ++i) pool->refcount[ids[i]] = 1;
+  rebuild_free(pool);
+  return PA_OK;
+}
+
+int kv_pool_retain(pa_kv_pool* pool, int32_t n, const int32_t* ids) {
+  int rc = check_ids(pool, n, ids, "kv_pool_retain");
+  if (rc) return rc;
+  for (int32_t i = 0; i < n; ++i)
+    if (pool->refcount[ids[i]] == 0)
+      return fail(PA_ESTATE, "kv_pool_retain: block %d is free", ids[i]);
+  for (int32_t i = 0; i < n; ++i) {
+    if (pool->refcount[ids[i]] == 0x7fffffff)
+      return fail(PA_ESTATE, "kv_pool_retain: reference count of block %d overflows", ids[i]);
+  }
+  for (int32_t i = 0; i < n; ++i) ++pool->refcount[ids[i]];
+  return PA_OK;
+}
+
+int kv_pool_release(pa_kv_pool* pool, int32_t n, const int32_t* ids) {
+  int rc = check_ids(pool, n, ids, "kv_pool_release");
+  if (rc) return rc;
+  std::vector<int32_t> count(pool->num_blocks, 0);
+  for (int32_t i = 0; i < n; ++i)
+    if (++count[ids[i]] > pool->refcount[ids[i]])
+      return fail(PA_ESTATE, "kv_pool_release: block %d released more often than retained", ids[i]);
+  bool freed = false;
+  for (int32_t i = 0; i < n; ++i) {
+    if (--pool->refcount[ids[i]] == 0) freed = true;
+  }
+  if (freed) rebuild_free(pool);
+  return PA_OK;
+}
+
+int kv_pool_num_free(const pa_kv_pool* pool, int32_t* n_out) {
+  if (!pool || !n_out) return fail(PA_EINVAL, "kv_pool_num_free: NULL argument");
+  *n_out = (int32_t)pool->free_stack.size();
+  return PA_OK;
+}
+
+int kv_pool_refcount(const pa_kv_pool* pool, int32_t id, int32_t* count_out) {
+  if (!pool || !count_out) return fail(PA_EINVAL, "kv_pool_refcount: NULL argument");
+  if (id < 0 || id >= pool->num_blocks)
+    return fail(PA_EINVAL, "kv_pool_refcount: id %d outside [0, %d)", id, pool->num_blocks);
+  *count_out = pool->refcount[id];
+  return PA_OK;
+}
+
+int kv_pool_layout(const pa_kv_pool* pool, int64_t elem_strides_out[4], int64_t* pool_bytes_out) {
+  if (!pool || !elem_strides_out) return fail(PA_EINVAL, "kv_pool_layout: NULL argument");
+  const int64_t d = pool->head_dim;
+  elem_strides_out[3] = 1;
+  elem_strides_out[2] = d;
+  elem_strides_out[1] = PA_BLOCK_SIZE * d;
+  elem_strides_out[0] = (int64_t)pool->num_kv_heads * PA_BLOCK_SIZE * d;
+  if (pool_bytes_out) *pool_bytes_out = elem_strides_out[0] * pool->num_blocks * 2;
+  return PA_OK;
+}
+
+int paged_attn_num_partitions(int32_t max_context_len, int32_t partition_size, int32_t* p_out) {
+  if (!p_out) return fail(PA_EINVAL, "paged_attn_num_partitions: p_out is NULL");
+  Plan pl;
+  int rc = plan(max_context_len, partition_size, &pl, "paged_attn_num_partitions");
+  if (rc) return rc;
+  *p_out = pl.num_parts;
+  return PA_OK;
+}
+
+int paged_attn_workspace_size(int32_t batch, int32_t num_q_heads, int32_t head_dim,
+                              int32_t max_context_len, int32_t partition_size,
+                              size_t* partial_out_bytes, size_t* partial_lse_bytes) {
+  if (!partial_out_bytes || !partial_lse_bytes)
+    return fail(PA_EINVAL, "paged_attn_workspace_size: NULL output pointer");
+  if (batch < 0 || num_q_heads <= 0 || head_dim <= 0)
+    return fail(PA_EINVAL, "paged_attn_workspace_size: bad geometry");
+  Plan pl;
+  int rc = plan(max_context_len, partition_size, &pl, "paged_attn_workspace_size");
+  if (rc) return rc;
+  if (pl.num_parts == 1) {
+    *partial_out_bytes = 0;
+    *partial_lse_bytes = 0;
+  } else {
+    const size_t rows = (size_t)batch * num_q_heads * pl.num_parts;
+    *partial_out_bytes = rows * head_dim * sizeof(float);
+    *partial_lse_bytes = rows * sizeof(float);
+  }
+  return PA_OK;
+}
+
+int paged_attn_decode(const pa_kv_pool* pool, const void* q, const int32_t* block_tables,
+                      int32_t bt_stride, const int32_t* context_lens, int32_t batch,
+                      int32_t num_q_heads, float scale, int32_t max_context_len,
+                      int32_t partition_size, void* out, float* partial_out, float* partial_lse,
+                      void* stream) {
+  return decode_impl(pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
+                     max_context_len, partition_size, out, partial_out, partial_lse, nullptr, 0,
+                     false, stream, "paged_attn_decode");
+}
+
+int paged_attn_decode_trace(const pa_kv_pool* pool, const void* q, const int32_t* block_tables,
+                            int32_t bt_stride, const int32_t* context_lens, int32_t batch,
+                            int32_t num_q_heads, float scale, int32_t max_context_len,
+                            int32_t partition_size, void* out, float* partial_out,
+                            float* partial_lse, int32_t* trace, int64_t trace_capacity,
+                            void* stream) {
+  return decode_impl(pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
+                     max_context_len, partition_size, out, partial_out, partial_lse, trace,
+                     trace_capacity, true, stream, "paged_attn_decode_trace");
+}
+
+int paged_attn_reduce(const float* partial_out, const float* partial_lse,
+                      const int32_t* context_lens, int32_t batch, int32_t num_q_heads,
+                      int32_t head_dim, int32_t partition_size, int32_t max_partitions, void* out,
+                      void* stream) {
+  const char* fn = "paged_attn_reduce";
+  if (batch < 0) return fail(PA_EINVAL, "%s: batch = %d < 0", fn, batch);
+  if (num_q_heads <= 0) return fail(PA_EINVAL, "%s: num_q_heads = %d <= 0", fn, num_q_heads);
+  if (head_dim != 64 && head_dim != 128)
+    return fail(PA_EUNSUPPORTED, "%s: head_dim = %d (supported: 64, 128)", fn, head_dim);
+  if (partition_size <= 0 || partition_size % PA_BLOCK_SIZE != 0)
+    return fail(PA_EINVAL, "%s: partition_size = %d is not a positive multiple of %d", fn,
+                partition_size, PA_BLOCK_SIZE);
+  if (max_partitions <= 0) return fail(PA_EINVAL, "%s: max_partitions = %d <= 0", fn, max_partitions);
+  if ((int64_t)batch * num_q_heads > 0x7fffffffLL) return fail(PA_EINVAL, "%s: grid too large", fn);
+  if (batch == 0) return PA_OK;
+  if (!partial_out || !partial_lse || !context_lens || !out)
+    return fail(PA_EINVAL, "%s: NULL buffer", fn);
+  if (!aligned(partial_out, 8) || !aligned(partial_lse, 4) || !aligned(context_lens, 4) ||
+      !aligned(out, 4))
+    return fail(PA_EINVAL, "%s: misaligned buffer", fn);
+  pa::ReduceParams p{};
+  p.part_o = partial_out;
+  p.part_lse = partial_lse;
+  p.context_lens = context_lens;
+  p.out = static_cast<uint16_t*>(out);
+  p.batch = batch;
+  p.num_q_heads = num_q_heads;
+  p.part_tokens = partition_size;
+  p.num_parts = max_partitions;
+  hipError_t e = pa::launch_reduce(p, head_dim, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
+  return PA_OK;
+}
+
+int pa_stream_copy(const void* src, void* dst, size_t bytes, void* stream) {
+  if (!src || !dst) return fail(PA_EINVAL, "pa_stream_copy: NULL pointer");
+  if (bytes % 16 != 0 || !aligned(src, 16) || !aligned(dst, 16))
+    return fail(PA_EINVAL, "pa_stream_copy: size and pointers must be 16-byte multiples/aligned");
+  hipError_t e = pa::launch_stream_copy(src, dst, bytes, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(PA_EHIP, "pa_stream_copy: kernel launch failed: %s", hipGetErrorString(e));
+  return PA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,51 @@
+// Kernel parameter blocks and launchers shared by the C-ABI layer and the
+// HIP kernels.  Host code fills these after validating every argument.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pa {
+
+struct DecodeParams {
+  const uint16_t* k_pool;        // bf16 [num_blocks][num_kv_heads][16][D]
+  const uint16_t* v_pool;        // same layout
+  const uint16_t* q;             // bf16 [batch][num_q_heads][D]
+  const int32_t* block_tables;   // [batch][bt_stride]
+  const int32_t* context_lens;   // [batch]
+  uint16_t* out;                 // bf16 [batch][num_q_heads][D] (single partition)
+  float* part_o;                 // fp32 [batch][num_q_heads][num_parts][D] (split)
+  float* part_lse;               // fp32 [batch][num_q_heads][num_parts]
+  int32_t* trace;                // index trace (trace variant only)
+  int32_t num_blocks;
+  int32_t num_kv_heads;
+  int32_t num_q_heads;
+  int32_t batch;
+  int32_t bt_stride;
+  int32_t max_ctx;
+  int32_t part_tokens;           // tokens per work item (a multiple of 16)
+  int32_t num_parts;             // partitions in the grid (1 = no split)
+  int32_t trace_tiles;           // trace slots per work item
+  float scale_log2;              // softmax scale * log2(e)
+};
+
+struct ReduceParams {
+  const float* part_o;
+  const float* part_lse;
+  const int32_t* context_lens;
+  uint16_t* out;
+  int32_t batch;
+  int32_t num_q_heads;
+  int32_t part_tokens;
+  int32_t num_parts;
+};
+
+// VALU split-KV decode (group size 4 or 8, head_dim 64 or 128).
+hipError_t launch_decode_valu(const DecodeParams& p, int head_dim, int group, bool trace,
+                              hipStream_t stream);
+// Log-sum-exp merge of split-KV partials into the bf16 output.
+hipError_t launch_reduce(const ReduceParams& p, int head_dim, hipStream_t stream);
+// Streaming device copy (measurement helper).
+hipError_t launch_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
+
+}  // namespace pa

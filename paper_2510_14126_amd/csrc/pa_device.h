@@ -1,0 +1,114 @@
+// Device-side helpers for the gfx950 (CDNA4) paged decode-attention kernels.
+//
+// Lane conventions used throughout: a wavefront has 64 lanes in four DPP
+// "rows" of 16.  Lane `l` belongs to row group `l >> 4` and row position
+// `l & 15`.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pa {
+
+constexpr int kBlockTokens = 16;  // tokens per KV block
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// ---- bf16 ------------------------------------------------------------------
+
+// Low / high bf16 of a packed pair, widened exactly to fp32.
+__device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t x) { return __uint_as_float(x & 0xffff0000u); }
+
+// fp32 -> bf16 bits with round-to-nearest-even; NaN stays a (quiet) NaN.
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+// Dot product of two bf16 pairs accumulated into fp32 (v_dot2c_f32_bf16).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                         __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+// 2^x on the hardware transcendental unit (v_exp_f32); exp2(-inf) = 0.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ---- cross-lane movement ---------------------------------------------------
+
+// DPP controls (gfx9 encoding).
+constexpr int kDppQuadXor1 = 0xB1;   // quad_perm [1,0,3,2]
+constexpr int kDppQuadXor2 = 0x4E;   // quad_perm [2,3,0,1]
+constexpr int kDppRowRor4 = 0x124;   // row_ror:4
+constexpr int kDppRowRor8 = 0x128;   // row_ror:8
+constexpr int kDppRowNewBcast = 0x150;  // row_newbcast:n = 0x150 + n
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xf, 0xf, true));
+}
+
+// Every lane of a 16-lane row gets the value of row position T.
+template <int T>
+__device__ __forceinline__ float row_bcast(float x) {
+  return dpp<kDppRowNewBcast + T>(x);
+}
+
+// Max / sum over the 16 lanes of each row; every lane receives the result.
+__device__ __forceinline__ float row_max16(float x) {
+  x = fmaxf(x, dpp<kDppQuadXor1>(x));
+  x = fmaxf(x, dpp<kDppQuadXor2>(x));
+  x = fmaxf(x, dpp<kDppRowRor4>(x));
+  x = fmaxf(x, dpp<kDppRowRor8>(x));
+  return x;
+}
+__device__ __forceinline__ float row_sum16(float x) {
+  x += dpp<kDppQuadXor1>(x);
+  x += dpp<kDppQuadXor2>(x);
+  x += dpp<kDppRowRor4>(x);
+  x += dpp<kDppRowRor8>(x);
+  return x;
+}
+
+// v_permlane32_swap: a' = [a(0..31), b(0..31)], b' = [a(32..63), b(32..63)].
+__device__ __forceinline__ void swap32(float& a, float& b) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_int(a), __float_as_int(b), false, false);
+  a = __int_as_float(r[0]);
+  b = __int_as_float(r[1]);
+}
+// v_permlane16_swap: a' rows = [a0, b0, a2, b2], b' rows = [a1, b1, a3, b3].
+__device__ __forceinline__ void swap16(float& a, float& b) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(a), __float_as_int(b), false, false);
+  a = __int_as_float(r[0]);
+  b = __int_as_float(r[1]);
+}
+
+// Reduce-scatter over the four row groups: every lane holds partials
+// x0..x3 (one per query row); afterwards the lanes of row group j hold the
+// sum over the four groups of x_j, at the same row position.
+__device__ __forceinline__ float reduce_scatter4(float x0, float x1, float x2, float x3) {
+  swap32(x0, x2);
+  swap32(x1, x3);
+  float y0 = x0 + x2;  // groups 0,1: row 0 | groups 2,3: row 2
+  float y1 = x1 + x3;  // groups 0,1: row 1 | groups 2,3: row 3
+  swap16(y0, y1);
+  return y0 + y1;      // group j: row j
+}
+
+// All-gather over the four row groups: lane (j, t) holds x_j(t); afterwards
+// every lane (*, t) holds x_0(t) .. x_3(t).
+__device__ __forceinline__ void allgather4(float x, float& r0, float& r1, float& r2, float& r3) {
+  float a = x, b = x;
+  swap32(a, b);        // a: rows of group j%2, b: rows of group j%2+2
+  float c = a, d = b;
+  swap16(a, c);        // a: x_0, c: x_1
+  swap16(b, d);        // b: x_2, d: x_3
+  r0 = a; r1 = c; r2 = b; r3 = d;
+}
+
+__device__ __forceinline__ int wave_uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+}  // namespace pa

@@ -1,0 +1,62 @@
+// Cross-split reduce: merge split-KV partials into the bf16 output.
+//
+// For sequence b and query head h the decode kernel left, per partition p,
+// the partition-normalised output o_p and its log-sum-exp lse_p (natural
+// log).  With P_b = ceil(ctx_b / S) partitions and M = max_p lse_p:
+//     w_p = exp(lse_p - M),   out = sum_p w_p o_p / sum_p w_p,
+// which is exactly softmax attention over the whole context.  One wavefront
+// per (b, h); lane l owns dims (D/64)*l ..; partitions are summed in order,
+// so the result is deterministic, and P_b = 1 reproduces o_0 bit for bit.
+#include "kernels.h"
+#include "pa_device.h"
+
+namespace pa {
+namespace {
+
+template <int D>
+__global__ void __launch_bounds__(64) reduce_kernel(const ReduceParams p) {
+  constexpr int DPL = D / 64;
+  const int lane = threadIdx.x;
+  const int bh = blockIdx.x;
+  const int b = bh / p.num_q_heads;
+  int n = p.context_lens[b];
+  n = n < 0 ? 0 : n;
+  int pb = n / p.part_tokens + (n % p.part_tokens != 0);
+  pb = pb > p.num_parts ? p.num_parts : pb;
+  const float* lse = p.part_lse + (size_t)bh * p.num_parts;
+  const float* po = p.part_o + (size_t)bh * p.num_parts * D + DPL * lane;
+
+  float mx = -__builtin_inff();
+  for (int q = 0; q < pb; ++q) mx = fmaxf(mx, lse[q]);
+  const float mref = (mx == -__builtin_inff()) ? 0.f : mx;
+  float wsum = 0.f, o[DPL];
+#pragma unroll
+  for (int d = 0; d < DPL; ++d) o[d] = 0.f;
+  for (int q = 0; q < pb; ++q) {
+    const float w = fast_exp2((lse[q] - mref) * kLog2e);
+    wsum += w;
+#pragma unroll
+    for (int d = 0; d < DPL; ++d) o[d] = fmaf(w, po[(size_t)q * D + d], o[d]);
+  }
+  const float inv = wsum > 0.f ? 1.0f / wsum : 0.f;
+  uint16_t* orow = p.out + (size_t)bh * D;
+  if constexpr (DPL == 2)
+    *reinterpret_cast<uint32_t*>(orow + 2 * lane) = bf16_rne(o[0] * inv) | (bf16_rne(o[1] * inv) << 16);
+  else
+    orow[lane] = (uint16_t)bf16_rne(o[0] * inv);
+}
+
+}  // namespace
+
+hipError_t launch_reduce(const ReduceParams& p, int head_dim, hipStream_t stream) {
+  const int64_t grid = (int64_t)p.batch * p.num_q_heads;
+  if (head_dim == 128)
+    hipLaunchKernelGGL(reduce_kernel<128>, dim3((unsigned)grid), dim3(64), 0, stream, p);
+  else if (head_dim == 64)
+    hipLaunchKernelGGL(reduce_kernel<64>, dim3((unsigned)grid), dim3(64), 0, stream, p);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace pa

@@ -1,0 +1,91 @@
+"""Device residency for one decode step: torch allocates, the library computes.
+
+``PagedBatch`` copies a generated workload's pools, queries, block tables and
+context lengths into device memory, registers the physical placement with
+the library's block pool (claim once, retain per extra reference), allocates
+the output and split-KV partials, and runs the two C-ABI calls of a step.
+Nothing here computes attention.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import binding
+
+
+def _dev(a: np.ndarray, device) -> torch.Tensor:
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a).to(device)
+
+
+class PagedBatch:
+    def __init__(self, w, device="cuda:0", partition_size: int | None = None,
+                 register_blocks: bool = True, k_pool=None, v_pool=None):
+        self.w = w
+        self.device = torch.device(device)
+        self.partition_size = w.partition_size if partition_size is None else partition_size
+        self.k = k_pool if k_pool is not None else _dev(w.k_pool, self.device)
+        self.v = v_pool if v_pool is not None else _dev(w.v_pool, self.device)
+        self.q = _dev(w.q, self.device)
+        self.bt = _dev(w.block_tables.astype(np.int32), self.device)
+        self.ctx = _dev(w.context_lens.astype(np.int32), self.device)
+        self.batch, self.hq, self.d = w.batch, w.num_q_heads, w.head_dim
+        self.max_ctx = w.max_context_len
+        self.out = torch.zeros((self.batch, self.hq, self.d), dtype=torch.int16, device=self.device)
+        self.pool = binding.kv_pool_create(w.num_blocks, binding.BLOCK_SIZE, w.num_kv_heads,
+                                           w.head_dim, self.k, self.v)
+        if register_blocks:
+            self.register_placement()
+        self.num_parts = binding.paged_attn_num_partitions(self.max_ctx, self.partition_size)
+        ob, lb = binding.paged_attn_workspace_size(self.batch, self.hq, self.d, self.max_ctx,
+                                                   self.partition_size)
+        self.part_o = torch.empty(ob // 4, dtype=torch.float32, device=self.device) if ob else None
+        self.part_lse = torch.empty(lb // 4, dtype=torch.float32, device=self.device) if lb else None
+
+    def register_placement(self) -> None:
+        """Claim every block the tables use; retain shared blocks once per extra user."""
+        w = self.w
+        nb = (w.context_lens.astype(np.int64) + 15) // 16
+        used = np.concatenate([w.block_tables[b, : nb[b]] for b in range(w.batch)]) \
+            if w.batch else np.zeros(0, np.int32)
+        ids, counts = np.unique(used, return_counts=True)
+        binding.kv_pool_claim(self.pool, ids.tolist())
+        extra = np.repeat(ids, counts - 1)
+        if extra.size:
+            binding.kv_pool_retain(self.pool, extra.tolist())
+
+    @property
+    def bt_stride(self) -> int:
+        return int(self.w.block_tables.shape[1])
+
+    def decode(self, stream=None, out=None) -> None:
+        binding.paged_attn_decode(self.pool, self.q, self.bt, self.bt_stride, self.ctx, self.batch,
+                                  self.hq, self.w.scale, self.max_ctx, self.partition_size,
+                                  self.out if out is None else out, self.part_o, self.part_lse,
+                                  stream)
+
+    def reduce(self, stream=None, out=None) -> None:
+        binding.paged_attn_reduce(self.part_o, self.part_lse, self.ctx, self.batch, self.hq, self.d,
+                                  self.partition_size, self.num_parts,
+                                  self.out if out is None else out, stream)
+
+    def run(self, stream=None) -> None:
+        """One decode step: split-KV decode, then the merge when it split."""
+        self.decode(stream)
+        if self.num_parts > 1:
+            self.reduce(stream)
+
+    def out_bits(self) -> np.ndarray:
+        return self.out.cpu().numpy().view(np.uint16)
+
+    def partials(self):
+        """Split-KV partials as numpy (o [B][Hq][P][D], lse [B][Hq][P])."""
+        o = self.part_o.view(self.batch, self.hq, self.num_parts, self.d).cpu().numpy()
+        l = self.part_lse.view(self.batch, self.hq, self.num_parts).cpu().numpy()
+        return o, l
+
+    def close(self) -> None:
+        self.pool.close()

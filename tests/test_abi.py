@@ -1,0 +1,191 @@
+"""Host-side tests of the C ABI: exports, allocator and argument validation.
+
+No kernel is launched here: every call either manipulates host metadata or
+fails validation before any HIP call, so these run without a GPU.
+"""
+import os
+import re
+
+import pytest
+
+from paper_2510_14126_amd import binding as pa
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+HEADER = os.path.join(HERE, "..", "include", "paged_attn.h")
+FAKE_K, FAKE_V = 0x10000, 0x20000     # aligned placeholder device addresses (never dereferenced)
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z_][a-z_0-9]*)\s*\(",
+                                 src, flags=re.M)))
+
+
+def test_header_and_library_agree():
+    names = declared_functions()
+    assert len(names) == 17, names
+    lib = pa.library()
+    for n in names:
+        assert hasattr(lib, n), f"library does not export {n}"
+    assert set(names) == set(pa.SIGNATURES)
+    assert pa.pa_version() >= 100
+
+
+def make_pool(nb=10, hkv=8, d=128):
+    return pa.kv_pool_create(nb, 16, hkv, d, FAKE_K, FAKE_V)
+
+
+def test_pool_create_validation():
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.kv_pool_create(10, 32, 8, 128, FAKE_K, FAKE_V)
+    assert e.value.code == pa.PA_EINVAL
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.kv_pool_create(10, 16, 8, 96, FAKE_K, FAKE_V)
+    assert e.value.code == pa.PA_EUNSUPPORTED
+    for bad in [(0, 16, 8, 128, FAKE_K, FAKE_V), (10, 16, 0, 128, FAKE_K, FAKE_V),
+                (10, 16, 8, 128, 0, FAKE_V), (10, 16, 8, 128, FAKE_K + 2, FAKE_V)]:
+        with pytest.raises(pa.PagedAttnError) as e:
+            pa.kv_pool_create(*bad)
+        assert e.value.code == pa.PA_EINVAL
+    assert "kv_pool_create" in pa.pa_last_error()
+
+
+def test_pool_layout():
+    p = make_pool(nb=7, hkv=8, d=128)
+    strides, nbytes = pa.kv_pool_layout(p)
+    assert strides == [8 * 16 * 128, 16 * 128, 128, 1]
+    assert nbytes == 7 * 8 * 16 * 128 * 2
+
+
+def test_alloc_release_and_exhaustion():
+    p = make_pool(nb=10)
+    assert pa.kv_pool_num_free(p) == 10
+    a = pa.kv_pool_alloc(p, 4)
+    assert a == [0, 1, 2, 3] and pa.kv_pool_num_free(p) == 6
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.kv_pool_alloc(p, 7)
+    assert e.value.code == pa.PA_ENOMEM and pa.kv_pool_num_free(p) == 6   # unchanged
+    b = pa.kv_pool_alloc(p, 6)
+    assert sorted(a + b) == list(range(10)) and pa.kv_pool_num_free(p) == 0
+    pa.kv_pool_release(p, [2, 5])
+    assert pa.kv_pool_num_free(p) == 2 and pa.kv_pool_refcount(p, 2) == 0
+    assert sorted(pa.kv_pool_alloc(p, 2)) == [2, 5]
+
+
+def test_shared_prefix_refcounts():
+    p = make_pool(nb=8)
+    prefix = pa.kv_pool_alloc(p, 3)
+    pa.kv_pool_retain(p, prefix)          # a second sequence maps the prefix
+    pa.kv_pool_retain(p, prefix)          # and a third
+    assert [pa.kv_pool_refcount(p, i) for i in prefix] == [3, 3, 3]
+    pa.kv_pool_release(p, prefix)
+    pa.kv_pool_release(p, prefix)
+    assert pa.kv_pool_num_free(p) == 5    # still held by the first sequence
+    pa.kv_pool_release(p, prefix)
+    assert pa.kv_pool_num_free(p) == 8
+
+
+def test_state_violations_change_nothing():
+    p = make_pool(nb=6)
+    ids = pa.kv_pool_alloc(p, 2)
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.kv_pool_release(p, [ids[0], ids[0]])   # double release in one call
+    assert e.value.code == pa.PA_ESTATE and pa.kv_pool_refcount(p, ids[0]) == 1
+    pa.kv_pool_release(p, [ids[0]])
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.kv_pool_release(p, [ids[0]])           # release of a free block
+    assert e.value.code == pa.PA_ESTATE
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.kv_pool_retain(p, [ids[1], ids[0]])    # retain of a free block
+    assert e.value.code == pa.PA_ESTATE and pa.kv_pool_refcount(p, ids[1]) == 1
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.kv_pool_release(p, [99])
+    assert e.value.code == pa.PA_EINVAL
+
+
+def test_claim_specific_blocks():
+    p = make_pool(nb=6)
+    pa.kv_pool_claim(p, [4, 1])
+    assert pa.kv_pool_num_free(p) == 4
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.kv_pool_claim(p, [0, 4])
+    assert e.value.code == pa.PA_ESTATE and pa.kv_pool_refcount(p, 0) == 0
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.kv_pool_claim(p, [2, 2])
+    assert e.value.code == pa.PA_ESTATE
+    assert pa.kv_pool_alloc(p, 4) == [0, 2, 3, 5]
+
+
+def test_partition_planning():
+    assert pa.paged_attn_num_partitions(0, 512) == 1
+    assert pa.paged_attn_num_partitions(512, 512) == 1
+    assert pa.paged_attn_num_partitions(513, 512) == 2
+    assert pa.paged_attn_num_partitions(32768, 512) == 64
+    assert pa.paged_attn_num_partitions(32768, 0) == 1
+    assert pa.paged_attn_workspace_size(4, 8, 64, 300, 512) == (0, 0)
+    assert pa.paged_attn_workspace_size(128, 64, 128, 32768, 512) == (128 * 64 * 64 * 128 * 4,
+                                                                      128 * 64 * 64 * 4)
+    with pytest.raises(pa.PagedAttnError):
+        pa.paged_attn_num_partitions(100, 24)
+
+
+def _decode(pool, **over):
+    args = dict(q=0x1000, block_tables=0x2000, bt_stride=4, context_lens=0x3000, batch=2,
+                num_q_heads=32, scale=0.088, max_context_len=64, partition_size=0, out=0x4000,
+                partial_out=None, partial_lse=None)
+    args.update(over)
+    pa.paged_attn_decode(pool, **args)
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(num_q_heads=24), pa.PA_EUNSUPPORTED),        # G = 3
+    (dict(num_q_heads=30), pa.PA_EINVAL),              # not a multiple of Hkv
+    (dict(batch=-1), pa.PA_EINVAL),
+    (dict(max_context_len=-5), pa.PA_EINVAL),
+    (dict(partition_size=20), pa.PA_EINVAL),
+    (dict(bt_stride=3), pa.PA_EINVAL),                 # ceil(64/16) = 4 needed
+    (dict(q=0x1008), pa.PA_EINVAL),                    # misaligned q
+    (dict(q=None), pa.PA_EINVAL),
+    (dict(out=None), pa.PA_EINVAL),                    # single partition needs out
+    (dict(max_context_len=1024, bt_stride=64, partition_size=512), pa.PA_EINVAL),  # no partials
+    (dict(scale=float("nan")), pa.PA_EINVAL),
+])
+def test_decode_validation(over, code):
+    p = make_pool()
+    with pytest.raises(pa.PagedAttnError) as e:
+        _decode(p, **over)
+    assert e.value.code == code, pa.pa_last_error()
+
+
+def test_empty_batch_is_a_no_op():
+    p = make_pool()
+    _decode(p, batch=0, q=None, block_tables=None, context_lens=None, out=None)
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(head_dim=96), pa.PA_EUNSUPPORTED),
+    (dict(partition_size=0), pa.PA_EINVAL),
+    (dict(max_partitions=0), pa.PA_EINVAL),
+    (dict(out=None), pa.PA_EINVAL),
+])
+def test_reduce_validation(over, code):
+    args = dict(partial_out=0x1000, partial_lse=0x2000, context_lens=0x3000, batch=2,
+                num_q_heads=8, head_dim=128, partition_size=512, max_partitions=3, out=0x4000)
+    args.update(over)
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.paged_attn_reduce(**args)
+    assert e.value.code == code
+
+
+def test_trace_capacity_checked():
+    p = make_pool()
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.paged_attn_decode_trace(p, 0x1000, 0x2000, 4, 0x3000, 2, 32, 0.1, 64, 0, 0x4000, None,
+                                   None, 0x5000, 10)
+    assert e.value.code == pa.PA_EINVAL and "trace_capacity" in pa.pa_last_error()
+
+
+def test_stream_copy_validation():
+    with pytest.raises(pa.PagedAttnError):
+        pa.pa_stream_copy(0x1000, 0x2000, 17)
