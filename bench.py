@@ -122,6 +122,69 @@ def traffic_from_profiles(workload_name):
     return float(m_tr.group(1))
 
 
+def ingest_counters(fetch_csv, write_csv, workload_name, kernel_prefix, command_note):
+    """Write the traffic summary from two rocprofv3 --pmc CSVs (FETCH_SIZE, WRITE_SIZE).
+
+    Each counter is scaled by what it reads for the calibration copy of
+    268435456 bytes each way (pa_stream_copy) in the same run.
+    """
+    import csv
+    import collections
+    from workloads import CONFIG_NAMES, build_config
+    k = [c for c, n in CONFIG_NAMES.items() if n == workload_name][0]
+    alg, _ = byte_accounting(build_config(k, values=False))
+    res = {}
+    for path, cname in ((fetch_csv, "FETCH_SIZE"), (write_csv, "WRITE_SIZE")):
+        per = collections.defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] == cname:
+                per[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+        copy = [v for n, v in per.items() if "stream_copy_kernel" in n][0]
+        kern = [(n, v) for n, v in per.items() if kernel_prefix in n]
+        if not kern:
+            raise SystemExit(f"no {kernel_prefix} dispatches in {path}")
+        name, vals = kern[0]
+        factor = (268435456 / 1024) / (sum(copy) / len(copy))
+        res[cname] = dict(kernel=name, n=len(vals), mean_kib=sum(vals) / len(vals),
+                          copy_kib=sum(copy) / len(copy), factor=factor)
+    f, wr = res["FETCH_SIZE"], res["WRITE_SIZE"]
+    fetched = f["mean_kib"] * f["factor"] * 1024
+    written = wr["mean_kib"] * wr["factor"] * 1024
+    out = os.path.join(PROFILE_DIR, f"decode_valu_{workload_name}_counters.md")
+    with open(out, "w") as fh:
+        fh.write(f"# HBM traffic counters: {f['kernel']} on the {workload_name} workload\n\n"
+                 f"Commands (run from /tmp with TMPDIR=/tmp):\n\n{command_note}\n\n"
+                 "Calibration: pa_stream_copy of 268435456 bytes read + 268435456 bytes written "
+                 "in the same runs.\n\n"
+                 f"| counter | calibration copy reads (KiB) | factor | kernel mean (KiB/dispatch) | "
+                 f"dispatches | scaled bytes/dispatch |\n|---|---|---|---|---|---|\n"
+                 f"| FETCH_SIZE | {f['copy_kib']:.1f} | {f['factor']:.4f} | {f['mean_kib']:.2f} | "
+                 f"{f['n']} | {fetched:,.0f} |\n"
+                 f"| WRITE_SIZE | {wr['copy_kib']:.1f} | {wr['factor']:.4f} | {wr['mean_kib']:.2f} | "
+                 f"{wr['n']} | {written:,.0f} |\n\n"
+                 f"algorithmic_bytes_per_launch: {alg}\n"
+                 f"traffic_bytes_per_launch: {fetched + written:.6e}\n"
+                 f"traffic_over_algorithmic: {(fetched + written) / alg:.4f}\n"
+                 f"kernel_source_sha256_16: {kernel_source_hash()}\n")
+    print(out)
+
+
+def ingest_stats(stats_csv, workload_name, command_note):
+    """Write the kernel-duration summary from a rocprofv3 --stats kernel_stats.csv."""
+    import csv
+    rows = list(csv.DictReader(open(stats_csv)))
+    out = os.path.join(PROFILE_DIR, f"kernels_{workload_name}_stats.md")
+    with open(out, "w") as fh:
+        fh.write(f"# Kernel durations on the {workload_name} workload (rocprofv3 --kernel-trace --stats)\n\n"
+                 f"Command (run from /tmp with TMPDIR=/tmp):\n\n{command_note}\n\n"
+                 "| kernel | calls | average (us) | min (us) | max (us) | share |\n|---|---|---|---|---|---|\n")
+        for r in rows:
+            fh.write(f"| `{r['Name'][:90]}` | {r['Calls']} | {float(r['AverageNs'])/1e3:.2f} | "
+                     f"{float(r['MinNs'])/1e3:.2f} | {float(r['MaxNs'])/1e3:.2f} | {float(r['Percentage']):.1f}% |\n")
+        fh.write(f"\nkernel_source_sha256_16: {kernel_source_hash()}\n")
+    print(out)
+
+
 # ---------------------------------------------------------------- GPU timing
 
 def main():
@@ -134,10 +197,23 @@ def main():
     ap.add_argument("--replicas", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--hot", action="store_true", help="also time steps on a single replica")
+    ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
+    ap.add_argument("--ingest-stats", metavar="KERNEL_STATS_CSV")
+    ap.add_argument("--command-note", default="")
     ap.add_argument("--profile-loop", type=int, default=0,
                     help="only run this many decode launches (plus one calibration copy) and exit; "
                          "for hardware-counter runs")
     args = ap.parse_args()
+
+    if args.ingest_counters or args.ingest_stats:
+        from workloads import CONFIG_NAMES
+        name = CONFIG_NAMES[args.config]
+        if args.ingest_counters:
+            ingest_counters(*args.ingest_counters, name, "decode_valu_kernel", args.command_note)
+        if args.ingest_stats:
+            ingest_stats(args.ingest_stats, name, args.command_note)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -228,9 +304,9 @@ def main():
     span_ms = ev[0][0].elapsed_time(ev[K - 1][2])
     ms_step = span_ms / K
 
-    # hot: one replica, same loop
+    # hot: one replica, same loop (optional)
     hot = []
-    for i in range(K):
+    for i in range(K if args.hot else 0):
         e0 = torch.cuda.Event(enable_timing=True); e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         pool, q = reps[0]
@@ -242,7 +318,7 @@ def main():
         e1.record(stream)
         hot.append((e0, e1))
     torch.cuda.synchronize()
-    hot_ms = float(np.mean([a.elapsed_time(b) for a, b in hot]))
+    hot_ms = float(np.mean([a.elapsed_time(b) for a, b in hot])) if hot else None
 
     # achievable copy bandwidth on this machine (read + write bytes)
     src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -299,7 +375,7 @@ def main():
         "tokens_per_s": round(w.batch * 1000.0 / ms_step, 1),
         "algorithmic_bytes_per_step": int(alg_bytes),
         "logical_kv_gbps_effective": round(logical_bytes / (ms_step * 1e-3) / 1e9, 2),
-        "hot_ms_per_step": round(hot_ms, 5),
+        "hot_ms_per_step": round(hot_ms, 5) if hot_ms is not None else None,
         "kernel_ms": {"decode_avg": round(dec_avg, 5), "reduce_avg": round(float(red_ms.mean()), 5)},
         "copy_probe_gbps": round(copy_gbps, 1),
         "pct_of_copy_probe": round(100 * value / copy_gbps, 2),
