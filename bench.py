@@ -37,16 +37,24 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 PROFILE_DIR = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = ["paper_2510_14126_amd/csrc/decode_valu.hip", "paper_2510_14126_amd/csrc/pa_device.h"]
+KERNEL_SOURCES = {
+    "decode_valu": ["paper_2510_14126_amd/csrc/decode_valu.hip", "paper_2510_14126_amd/csrc/pa_device.h"],
+    "decode_mfma": ["paper_2510_14126_amd/csrc/decode_mfma.hip", "paper_2510_14126_amd/csrc/pa_device.h"],
+}
+
+
+def decode_kernel_of(w) -> str:
+    """Which decode kernel the library launches for this geometry."""
+    return "decode_mfma" if (w.group == 8 and w.head_dim == 128) else "decode_valu"
 
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(kernel: str = "decode_valu") -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in KERNEL_SOURCES[kernel]:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -108,16 +116,16 @@ def cpu_baseline(w, alg_bytes, min_seconds=10.0):
 
 # ------------------------------------------------------------------ traffic
 
-def traffic_from_profiles(workload_name):
+def traffic_from_profiles(workload_name, kernel="decode_valu"):
     """Counter-derived HBM bytes per decode launch, if the profile summary was
     taken on the current kernel source; else None."""
-    path = os.path.join(PROFILE_DIR, f"decode_valu_{workload_name}_counters.md")
+    path = os.path.join(PROFILE_DIR, f"{kernel}_{workload_name}_counters.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
     m_src = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
     m_tr = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not m_src or not m_tr or m_src.group(1) != kernel_source_hash():
+    if not m_src or not m_tr or m_src.group(1) != kernel_source_hash(kernel):
         return None
     return float(m_tr.group(1))
 
@@ -140,7 +148,7 @@ def ingest_counters(fetch_csv, write_csv, workload_name, kernel_prefix, command_
             if r["Counter_Name"] == cname:
                 per[r["Kernel_Name"]].append(float(r["Counter_Value"]))
         copy = [v for n, v in per.items() if "stream_copy_kernel" in n][0]
-        kern = [(n, v) for n, v in per.items() if kernel_prefix in n]
+        kern = [(n, v) for n, v in per.items() if kernel_prefix + "_" in n]
         if not kern:
             raise SystemExit(f"no {kernel_prefix} dispatches in {path}")
         name, vals = kern[0]
@@ -150,7 +158,7 @@ def ingest_counters(fetch_csv, write_csv, workload_name, kernel_prefix, command_
     f, wr = res["FETCH_SIZE"], res["WRITE_SIZE"]
     fetched = f["mean_kib"] * f["factor"] * 1024
     written = wr["mean_kib"] * wr["factor"] * 1024
-    out = os.path.join(PROFILE_DIR, f"decode_valu_{workload_name}_counters.md")
+    out = os.path.join(PROFILE_DIR, f"{kernel_prefix}_{workload_name}_counters.md")
     with open(out, "w") as fh:
         fh.write(f"# HBM traffic counters: {f['kernel']} on the {workload_name} workload\n\n"
                  f"Commands (run from /tmp with TMPDIR=/tmp):\n\n{command_note}\n\n"
@@ -165,7 +173,7 @@ def ingest_counters(fetch_csv, write_csv, workload_name, kernel_prefix, command_
                  f"algorithmic_bytes_per_launch: {alg}\n"
                  f"traffic_bytes_per_launch: {fetched + written:.6e}\n"
                  f"traffic_over_algorithmic: {(fetched + written) / alg:.4f}\n"
-                 f"kernel_source_sha256_16: {kernel_source_hash()}\n")
+                 f"kernel_source_sha256_16: {kernel_source_hash(kernel_prefix)}\n")
     print(out)
 
 
@@ -181,7 +189,8 @@ def ingest_stats(stats_csv, workload_name, command_note):
         for r in rows:
             fh.write(f"| `{r['Name'][:90]}` | {r['Calls']} | {float(r['AverageNs'])/1e3:.2f} | "
                      f"{float(r['MinNs'])/1e3:.2f} | {float(r['MaxNs'])/1e3:.2f} | {float(r['Percentage']):.1f}% |\n")
-        fh.write(f"\nkernel_source_sha256_16: {kernel_source_hash()}\n")
+        fh.write("".join(f"\nkernel_source_sha256_16 ({k}): {kernel_source_hash(k)}"
+                         for k in KERNEL_SOURCES) + "\n")
     print(out)
 
 
@@ -210,7 +219,9 @@ def main():
         from workloads import CONFIG_NAMES
         name = CONFIG_NAMES[args.config]
         if args.ingest_counters:
-            ingest_counters(*args.ingest_counters, name, "decode_valu_kernel", args.command_note)
+            from workloads import build_config
+            kern = decode_kernel_of(build_config(args.config, values=False))
+            ingest_counters(*args.ingest_counters, name, kern, args.command_note)
         if args.ingest_stats:
             ingest_stats(args.ingest_stats, name, args.command_note)
         return
@@ -350,7 +361,8 @@ def main():
     dec_avg = float(dec_ms.mean())
     achieved = alg_bytes / (dec_avg * 1e-3) / 1e9
     value = alg_bytes / (ms_step * 1e-3) / 1e9
-    traffic = traffic_from_profiles(w.name)
+    kern = decode_kernel_of(w)
+    traffic = traffic_from_profiles(w.name, kern)
     line = {
         "metric": "paged decode-attention KV GB/s (algorithmic bytes) and % of HBM peak; "
                   "decode steps/s per batch",
@@ -384,7 +396,9 @@ def main():
                               "worst_row_rel_l2": rep.worst_row_rel_l2},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": traffic, "kernel": "decode_valu_kernel<128,4>",
+                     "traffic": traffic,
+                     "kernel": ("decode_mfma_g8_kernel" if kern == "decode_mfma"
+                                else f"decode_valu_kernel<{w.head_dim},{w.group}>"),
                      "bytes_per_launch": int(alg_bytes)},
         "cpu_baseline": cpu,
     }

@@ -146,8 +146,12 @@ int decode_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tabl
   p.num_parts = pl.num_parts;
   p.trace_tiles = trace_tiles;
   p.scale_log2 = scale * 1.4426950408889634f;
-  hipError_t e = pa::launch_decode_valu(p, pool->head_dim, group, tracing,
-                                        static_cast<hipStream_t>(stream));
+  // GQA groups of 8 at head_dim 128 form dense 16x16 tiles: matrix cores;
+  // everything else runs on VALU dot products.
+  hipError_t e = (group == 8 && pool->head_dim == 128)
+                     ? pa::launch_decode_mfma(p, tracing, static_cast<hipStream_t>(stream))
+                     : pa::launch_decode_valu(p, pool->head_dim, group, tracing,
+                                              static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
   return PA_OK;
 }

@@ -43,6 +43,8 @@ struct ReduceParams {
 // VALU split-KV decode (group size 4 or 8, head_dim 64 or 128).
 hipError_t launch_decode_valu(const DecodeParams& p, int head_dim, int group, bool trace,
                               hipStream_t stream);
+// MFMA split-KV decode for group size 8, head_dim 128.
+hipError_t launch_decode_mfma(const DecodeParams& p, bool trace, hipStream_t stream);
 // Log-sum-exp merge of split-KV partials into the bf16 output.
 hipError_t launch_reduce(const ReduceParams& p, int head_dim, hipStream_t stream);
 // Streaming device copy (measurement helper).

@@ -103,16 +103,18 @@ def test_edge_contexts(S, d, hq, hkv):
     assert_gate(gpu_out(w, S), decode_workload(w)[0], f"edges S={S}")
 
 
+@pytest.mark.parametrize("hq", [8, 16])
 @pytest.mark.parametrize("S", [0, 64])
-def test_empty_and_single_token_contexts(S):
-    say(f"ctx 0 and 1, S={S}")
-    case = logical_case(9, 5, 8, 2, 128, [0, 1, 33, 1, 200])
+def test_empty_and_single_token_contexts(S, hq):
+    say(f"ctx 0 and 1, S={S} Hq={hq}")
+    case = logical_case(9, 5, hq, 2, 128, [0, 1, 33, 1, 200])
     w = page_case(case, 3)
     out = gpu_out(w, S)
+    G = hq // 2
     assert np.all(out[0] & 0x7FFF == 0), "empty context must give zeros"
     for b in (1, 3):
-        for h in range(8):
-            assert np.array_equal(out[b, h], case.v[b][h // 4, 0]), "ctx=1 must return V exactly"
+        for h in range(hq):
+            assert np.array_equal(out[b, h], case.v[b][h // G, 0]), "ctx=1 must return V exactly"
     assert_gate(out[2:3], decode_workload(w, seqs=[2])[0], "ctx 33 beside empty rows")
 
 
@@ -164,14 +166,15 @@ with open(os.path.join(HERE, "golden", "hand_cases.json")) as f:
     HAND = json.load(f)["cases"]
 
 
+@pytest.mark.parametrize("d,group", [(64, 4), (128, 8)], ids=["valu", "mfma"])
 @pytest.mark.parametrize("case", HAND, ids=[c["name"] for c in HAND])
-def test_hand_cases(case):
-    say(f"hand case {case['name']}")
-    w = _embed(case["q_bits"], case["K_bits"], case["V_bits"], case["scale"])
+def test_hand_cases(case, d, group):
+    say(f"hand case {case['name']} D={d} G={group}")
+    w = _embed(case["q_bits"], case["K_bits"], case["V_bits"], case["scale"], d=d, group=group)
     out = gpu_out(w)
     R = len(case["q"])
     ncol = len(case["out"][0])
-    for r in range(4):
+    for r in range(group):
         got = bf16_to_f64(out[0, r, :ncol])
         want = np.array(case["out"][r % R])
         np.testing.assert_allclose(got, want, rtol=2 ** -8, atol=0)
@@ -179,7 +182,7 @@ def test_hand_cases(case):
         if "out_bf16_bits" in case:
             assert list(out[0, r, :ncol]) == case["out_bf16_bits"][r % R], "bf16 output must use RNE"
     if case["name"] in ("single_token", "argmax_group2") or case["name"].startswith("rne"):
-        for r in range(4):
+        for r in range(group):
             want_bits = f32_to_bf16_bits(np.float32(case["out"][r % R]))
             assert np.array_equal(out[0, r, :ncol], want_bits)
 
@@ -210,12 +213,13 @@ def _argmax_workload(ctx, targets, d=128, hq=32, hkv=8, seed=3, poison=True):
     return w, want
 
 
+@pytest.mark.parametrize("hq", [32, 64])
 @pytest.mark.parametrize("S", [0, 64, 512])
-def test_argmax_reads_exact_slot(S):
+def test_argmax_reads_exact_slot(S, hq):
     ctx = [1, 40, 513, 1024, 1024, 700, 17]
     targets = [0, 39, 512, 511, 0, 64, 16]
-    say(f"argmax slot selection S={S}")
-    w, want = _argmax_workload(ctx, targets)
+    say(f"argmax slot selection S={S} Hq={hq}")
+    w, want = _argmax_workload(ctx, targets, hq=hq)
     out = gpu_out(w, S)
     for b, (pid, r) in enumerate(want):
         got = bf16_to_f64(out[b, :, :3])
@@ -234,26 +238,29 @@ def test_poison_past_context_is_never_used():
         assert np.isfinite(bf16_to_f64(dirty)).all()
 
 
-def test_block_permutation_bit_identical():
-    say("physical block permutation")
-    w = page_case(logical_case(31, 6, 32, 8, 128, [900, 40, 600, 33, 48, 2048], prefix_len=32), 5)
+@pytest.mark.parametrize("hq", [32, 64])
+def test_block_permutation_bit_identical(hq):
+    say(f"physical block permutation Hq={hq}")
+    w = page_case(logical_case(31, 6, hq, 8, 128, [900, 40, 600, 33, 48, 2048], prefix_len=32), 5)
     base = gpu_out(w, 512)
     for s in range(2):
         assert np.array_equal(base, gpu_out(permute_blocks(w, 60 + s), 512))
 
 
-def test_shared_prefix_equals_duplicated_bit_identical():
-    say("shared prefix vs duplicated copies")
-    w = page_case(logical_case(32, 6, 32, 8, 128, [900, 600, 2100, 520, 515, 1000], prefix_len=512), 6)
+@pytest.mark.parametrize("hq", [32, 64])
+def test_shared_prefix_equals_duplicated_bit_identical(hq):
+    say(f"shared prefix vs duplicated copies Hq={hq}")
+    w = page_case(logical_case(32, 6, hq, 8, 128, [900, 600, 2100, 520, 515, 1000], prefix_len=512), 6)
     assert w.meta["shared_blocks"] == 32
     a = gpu_out(w, 512)
     b = gpu_out(duplicate_shared_blocks(w), 512)
     assert np.array_equal(a, b)
 
 
-def test_repeat_runs_bit_identical():
-    say("determinism")
-    w = build_config(2)
+@pytest.mark.parametrize("k", [2, 1])
+def test_repeat_runs_bit_identical(k):
+    say(f"determinism config {k}")
+    w = build_config(k)
     from paper_2510_14126_amd.device import PagedBatch
     pb = PagedBatch(w, DEV)
     outs = []
@@ -266,9 +273,10 @@ def test_repeat_runs_bit_identical():
     assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
 
 
-def test_single_partition_through_reduce_matches_single_pass():
-    say("P_b = 1 through the reduce vs single pass")
-    case = logical_case(33, 3, 32, 8, 128, [2000, 300, 512])
+@pytest.mark.parametrize("hq", [32, 64])
+def test_single_partition_through_reduce_matches_single_pass(hq):
+    say(f"P_b = 1 through the reduce vs single pass Hq={hq}")
+    case = logical_case(33, 3, hq, 8, 128, [2000, 300, 512])
     w = page_case(case, 8)
     split = gpu_out(w, 512)            # sequence 0 splits, 1 and 2 have one partition
     single = gpu_out(w, 0)
@@ -315,12 +323,13 @@ def expected_trace(w, part_tokens, num_parts):
     return exp
 
 
+@pytest.mark.parametrize("hq", [32, 64])
 @pytest.mark.parametrize("S", [0, 64, 512])
-def test_index_trace_bit_exact(S):
+def test_index_trace_bit_exact(S, hq):
     from paper_2510_14126_amd import binding
     from paper_2510_14126_amd.device import PagedBatch
-    say(f"index trace S={S}")
-    case = logical_case(40, 5, 32, 8, 128, [1, 16, 17, 700, 1300], prefix_len=0)
+    say(f"index trace S={S} Hq={hq}")
+    case = logical_case(40, 5, hq, 8, 128, [1, 16, 17, 700, 1300], prefix_len=0)
     w = page_case(case, 41, table_pad=3)
     pb = PagedBatch(w, DEV, partition_size=S)
     P = pb.num_parts
@@ -362,3 +371,23 @@ def test_gate_rejects_planted_mistakes_on_gpu():
         bt[b, [0, last]] = bt[b, [last, 0]]
     swapped = Workload(**{**w.__dict__}); swapped.block_tables = bt
     assert not compare(gpu_out(swapped), truth).passed
+
+
+@pytest.mark.parametrize("hq", [32, 64])
+@pytest.mark.parametrize("S", [0, 512])
+def test_growing_scores_force_rescales(S, hq):
+    """Scores rising along the context make the running max grow many times."""
+    say(f"growing scores S={S} Hq={hq}")
+    case = logical_case(60, 3, hq, 8, 128, [2500, 1200, 777])
+    for b in range(3):
+        n = case.k[b].shape[1]
+        k = bf16_to_f64(case.k[b]).astype(np.float32)
+        k[:, :, 0] = np.arange(n, dtype=np.float32)[None, :] / 24.0
+        case.k[b] = f32_to_bf16_bits(k)
+    qf = bf16_to_f64(case.q).astype(np.float32)
+    qf[:, :, 0] = 6.0
+    case.q[:] = f32_to_bf16_bits(qf)
+    w = page_case(case, 61)
+    ref, lse = decode_workload(w)
+    assert np.ptp(lse) > 10
+    assert_gate(gpu_out(w, S), ref, f"growing scores S={S} Hq={hq}")
