@@ -90,7 +90,7 @@ int32_t pa_version(void);
  *   block_size    must be 16 (tokens per block)
  *   num_kv_heads  1 .. 64
  *   head_dim      64 or 128 (others: PA_EUNSUPPORTED)
- *   k_pool,v_pool device pointers, 256-byte aligned, each holding
+ *   k_pool,v_pool device pointers, 16-byte aligned, each holding
  *                 num_blocks*num_kv_heads*16*head_dim bf16 values
  *   out           receives the handle; *out is untouched on error.
  * All blocks start free. */
@@ -178,6 +178,59 @@ int paged_attn_reduce(const float *partial_out, const float *partial_lse,
                       const int32_t *context_lens, int32_t batch, int32_t num_q_heads,
                       int32_t head_dim, int32_t partition_size, int32_t max_partitions,
                       void *out, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Shared-prefix (cascade) decode.
+ *
+ * Every sequence of a stage pool's batch starts with the same prompt -- the
+ * schema that all SQL-generator calls and all fixer retries share (Cortex
+ * paper, section 1; section 2 "Cortex Benefits") -- stored once as the same
+ * physical blocks in every block table.  The cascade computes attention over
+ * that prefix once per KV head for all B*G query rows together, as dense
+ * matrix-core tiles, and over each sequence's remaining tokens with the
+ * per-sequence kernels; paged_attn_reduce_cascade merges both kinds of
+ * partials by log-sum-exp into the same result as paged_attn_decode.
+ * ------------------------------------------------------------------------- */
+
+/* Partial-buffer sizes of a cascade step and the partition count per
+ * (sequence, head) (pass it as max_partitions to the reduce).
+ *   partition_size         tokens per partition after the prefix: a positive
+ *                          multiple of 16
+ *   prefix_len             shared prefix tokens: a multiple of 16, 0 allowed,
+ *                          at most max_context_len
+ *   prefix_partition_size  tokens per prefix partition: a multiple of 16 in
+ *                          [16, 1024] */
+int paged_attn_cascade_workspace_size(int32_t batch, int32_t num_q_heads, int32_t head_dim,
+                                      int32_t max_context_len, int32_t partition_size,
+                                      int32_t prefix_len, int32_t prefix_partition_size,
+                                      size_t *partial_out_bytes, size_t *partial_lse_bytes,
+                                      int32_t *max_partitions_out);
+
+/* First half of a cascade step: writes the (o, lse) partials of the prefix
+ * partitions and of the per-sequence partitions after the prefix into
+ * partial_out / partial_lse (sizes from paged_attn_cascade_workspace_size).
+ * The caller guarantees that entries 0 .. prefix_len/16 - 1 of every block
+ * table row are the same physical blocks; the prefix pass reads them from
+ * row 0.  A sequence shorter than prefix_len attends only to its own
+ * context.  The prefix pass needs head_dim 128; other arguments as in
+ * paged_attn_decode.  Follow with paged_attn_reduce_cascade on the same
+ * stream. */
+int paged_attn_decode_cascade(const pa_kv_pool *pool, const void *q, const int32_t *block_tables,
+                              int32_t bt_stride, const int32_t *context_lens, int32_t batch,
+                              int32_t num_q_heads, float scale, int32_t max_context_len,
+                              int32_t partition_size, int32_t prefix_len,
+                              int32_t prefix_partition_size, float *partial_out,
+                              float *partial_lse, void *stream);
+
+/* Second half of a cascade step: merges, for each (b, h), the prefix
+ * partials and the ceil((ctx_b - prefix_len) / partition_size) partials after
+ * it into the bf16 output.  Arguments as in paged_attn_decode_cascade and
+ * paged_attn_reduce. */
+int paged_attn_reduce_cascade(const float *partial_out, const float *partial_lse,
+                              const int32_t *context_lens, int32_t batch, int32_t num_q_heads,
+                              int32_t head_dim, int32_t partition_size, int32_t prefix_len,
+                              int32_t prefix_partition_size, int32_t max_partitions, void *out,
+                              void *stream);
 
 /* Index-trace variant of paged_attn_decode, for verifying block-table and
  * context-length handling.  It runs the same gather code and, in addition,

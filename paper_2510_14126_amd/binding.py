@@ -46,6 +46,13 @@ SIGNATURES = {
     "paged_attn_decode_trace": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32,
                                          _i32, _vp, _vp, _vp, _vp, _i64, _vp]),
     "pa_stream_copy": (_c_int, [_vp, _vp, _sz, _vp]),
+    "paged_attn_cascade_workspace_size": (_c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _i32,
+                                                   ctypes.POINTER(_sz), ctypes.POINTER(_sz),
+                                                   _pi32]),
+    "paged_attn_decode_cascade": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32,
+                                           _i32, _i32, _i32, _vp, _vp, _vp]),
+    "paged_attn_reduce_cascade": (_c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32,
+                                           _i32, _vp, _vp]),
 }
 
 
@@ -233,3 +240,33 @@ def paged_attn_decode_trace(pool: KVPool, q, block_tables, bt_stride, context_le
 
 def pa_stream_copy(src, dst, nbytes, stream=None) -> None:
     _check(_lib.pa_stream_copy(_ptr(src), _ptr(dst), nbytes, _ptr(stream)))
+
+
+def paged_attn_cascade_workspace_size(batch, num_q_heads, head_dim, max_context_len,
+                                      partition_size, prefix_len, prefix_partition_size):
+    """Returns (partial_out bytes, partial_lse bytes, max_partitions)."""
+    a, b, m = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_int32()
+    _check(_lib.paged_attn_cascade_workspace_size(batch, num_q_heads, head_dim, max_context_len,
+                                                  partition_size, prefix_len,
+                                                  prefix_partition_size, ctypes.byref(a),
+                                                  ctypes.byref(b), ctypes.byref(m)))
+    return a.value, b.value, m.value
+
+
+def paged_attn_decode_cascade(pool: KVPool, q, block_tables, bt_stride, context_lens, batch,
+                              num_q_heads, scale, max_context_len, partition_size, prefix_len,
+                              prefix_partition_size, partial_out, partial_lse, stream=None) -> None:
+    _check(_lib.paged_attn_decode_cascade(pool._handle(), _ptr(q), _ptr(block_tables), bt_stride,
+                                          _ptr(context_lens), batch, num_q_heads, scale,
+                                          max_context_len, partition_size, prefix_len,
+                                          prefix_partition_size, _ptr(partial_out),
+                                          _ptr(partial_lse), _ptr(stream)))
+
+
+def paged_attn_reduce_cascade(partial_out, partial_lse, context_lens, batch, num_q_heads,
+                              head_dim, partition_size, prefix_len, prefix_partition_size,
+                              max_partitions, out, stream=None) -> None:
+    _check(_lib.paged_attn_reduce_cascade(_ptr(partial_out), _ptr(partial_lse),
+                                          _ptr(context_lens), batch, num_q_heads, head_dim,
+                                          partition_size, prefix_len, prefix_partition_size,
+                                          max_partitions, _ptr(out), _ptr(stream)))

@@ -1,7 +1,7 @@
 // C ABI of the paged decode-attention library: KV block pool allocator,
 // argument validation and launch planning.  Every check runs on the host
 // before any HIP call, so all validation paths work without a GPU.
-#include "../../include/paged_attn.h"
+#include "paged_attn.h"
 #include "kernels.h"
 
 #include <hip/hip_runtime.h>
@@ -77,36 +77,84 @@ int plan(int32_t max_context_len, int32_t partition_size, Plan* out, const char*
   return PA_OK;
 }
 
-int decode_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tables,
-                int32_t bt_stride, const int32_t* context_lens, int32_t batch,
-                int32_t num_q_heads, float scale, int32_t max_context_len, int32_t partition_size,
-                void* out, float* partial_out, float* partial_lse, int32_t* trace,
-                int64_t trace_capacity, bool tracing, void* stream, const char* fn) {
-  if (!pool) return fail(PA_EINVAL, "%s: pool is NULL", fn);
-  if (batch < 0) return fail(PA_EINVAL, "%s: batch = %d < 0", fn, batch);
-  if (num_q_heads <= 0 || num_q_heads % pool->num_kv_heads != 0)
+struct DecodeArgs {
+  const pa_kv_pool* pool;
+  const void* q;
+  const int32_t* block_tables;
+  int32_t bt_stride;
+  const int32_t* context_lens;
+  int32_t batch;
+  int32_t num_q_heads;
+  float scale;
+  int32_t max_context_len;
+};
+
+// Checks shared by every decode entry point; fills the group size.
+int validate_decode(const DecodeArgs& a, int32_t* group, const char* fn) {
+  if (!a.pool) return fail(PA_EINVAL, "%s: pool is NULL", fn);
+  if (a.batch < 0) return fail(PA_EINVAL, "%s: batch = %d < 0", fn, a.batch);
+  if (a.num_q_heads <= 0 || a.num_q_heads % a.pool->num_kv_heads != 0)
     return fail(PA_EINVAL, "%s: num_q_heads = %d is not a positive multiple of num_kv_heads = %d",
-                fn, num_q_heads, pool->num_kv_heads);
-  const int32_t group = num_q_heads / pool->num_kv_heads;
-  if (group != 4 && group != 8)
-    return fail(PA_EUNSUPPORTED, "%s: query heads per KV head = %d (supported: 4, 8)", fn, group);
-  if (!(scale == scale) || scale == __builtin_inff() || scale == -__builtin_inff())
+                fn, a.num_q_heads, a.pool->num_kv_heads);
+  *group = a.num_q_heads / a.pool->num_kv_heads;
+  if (*group != 4 && *group != 8)
+    return fail(PA_EUNSUPPORTED, "%s: query heads per KV head = %d (supported: 4, 8)", fn, *group);
+  if (!(a.scale == a.scale) || a.scale == __builtin_inff() || a.scale == -__builtin_inff())
     return fail(PA_EINVAL, "%s: scale is not finite", fn);
-  Plan pl;
-  int rc = plan(max_context_len, partition_size, &pl, fn);
-  if (rc) return rc;
-  const int64_t need_bt = ((int64_t)max_context_len + PA_BLOCK_SIZE - 1) / PA_BLOCK_SIZE;
-  if (bt_stride < need_bt || bt_stride < 0)
-    return fail(PA_EINVAL, "%s: bt_stride = %d < ceil(max_context_len / 16) = %lld", fn, bt_stride,
-                (long long)need_bt);
-  const int64_t grid = (int64_t)pl.num_parts * batch * pool->num_kv_heads;
-  if (grid > 0x7fffffffLL) return fail(PA_EINVAL, "%s: grid of %lld workgroups is too large", fn, (long long)grid);
-  if (batch == 0) return PA_OK;
-  if (!q || !block_tables || !context_lens)
+  if (a.max_context_len < 0)
+    return fail(PA_EINVAL, "%s: max_context_len = %d < 0", fn, a.max_context_len);
+  const int64_t need_bt = ((int64_t)a.max_context_len + PA_BLOCK_SIZE - 1) / PA_BLOCK_SIZE;
+  if (a.bt_stride < need_bt || a.bt_stride < 0)
+    return fail(PA_EINVAL, "%s: bt_stride = %d < ceil(max_context_len / 16) = %lld", fn,
+                a.bt_stride, (long long)need_bt);
+  if (a.batch == 0) return PA_OK;
+  if (!a.q || !a.block_tables || !a.context_lens)
     return fail(PA_EINVAL, "%s: q, block_tables and context_lens must be non-NULL", fn);
-  if (!aligned(q, 16)) return fail(PA_EINVAL, "%s: q is not 16-byte aligned", fn);
-  if (!aligned(block_tables, 4) || !aligned(context_lens, 4))
+  if (!aligned(a.q, 16)) return fail(PA_EINVAL, "%s: q is not 16-byte aligned", fn);
+  if (!aligned(a.block_tables, 4) || !aligned(a.context_lens, 4))
     return fail(PA_EINVAL, "%s: block_tables/context_lens are not 4-byte aligned", fn);
+  return PA_OK;
+}
+
+pa::DecodeParams decode_params(const DecodeArgs& a) {
+  pa::DecodeParams p{};
+  p.k_pool = a.pool->k;
+  p.v_pool = a.pool->v;
+  p.q = static_cast<const uint16_t*>(a.q);
+  p.block_tables = a.block_tables;
+  p.context_lens = a.context_lens;
+  p.num_blocks = a.pool->num_blocks;
+  p.num_kv_heads = a.pool->num_kv_heads;
+  p.num_q_heads = a.num_q_heads;
+  p.batch = a.batch;
+  p.bt_stride = a.bt_stride;
+  p.max_ctx = a.max_context_len;
+  p.scale_log2 = a.scale * 1.4426950408889634f;
+  return p;
+}
+
+hipError_t launch_decode(const pa::DecodeParams& p, const pa_kv_pool* pool, int32_t group,
+                         bool tracing, void* stream) {
+  // GQA groups of 8 at head_dim 128 form dense 16x16 tiles: matrix cores;
+  // everything else runs on VALU dot products.
+  return (group == 8 && pool->head_dim == 128)
+             ? pa::launch_decode_mfma(p, tracing, static_cast<hipStream_t>(stream))
+             : pa::launch_decode_valu(p, pool->head_dim, group, tracing,
+                                      static_cast<hipStream_t>(stream));
+}
+
+int decode_impl(const DecodeArgs& a, int32_t partition_size, void* out, float* partial_out,
+                float* partial_lse, int32_t* trace, int64_t trace_capacity, bool tracing,
+                void* stream, const char* fn) {
+  int32_t group = 0;
+  int rc = validate_decode(a, &group, fn);
+  if (rc) return rc;
+  Plan pl;
+  rc = plan(a.max_context_len, partition_size, &pl, fn);
+  if (rc) return rc;
+  const int64_t grid = (int64_t)pl.num_parts * a.batch * a.pool->num_kv_heads;
+  if (grid > 0x7fffffffLL) return fail(PA_EINVAL, "%s: grid of %lld workgroups is too large", fn, (long long)grid);
+  if (a.batch == 0) return PA_OK;
   const bool split = pl.num_parts > 1;
   if (!split) {
     if (!out) return fail(PA_EINVAL, "%s: out is NULL (single partition)", fn);
@@ -125,34 +173,53 @@ int decode_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tabl
       return fail(PA_EINVAL, "%s: trace_capacity %lld < %lld int32 values", fn,
                   (long long)trace_capacity, (long long)need);
   }
-
-  pa::DecodeParams p{};
-  p.k_pool = pool->k;
-  p.v_pool = pool->v;
-  p.q = static_cast<const uint16_t*>(q);
-  p.block_tables = block_tables;
-  p.context_lens = context_lens;
+  pa::DecodeParams p = decode_params(a);
   p.out = static_cast<uint16_t*>(out);
   p.part_o = partial_out;
   p.part_lse = partial_lse;
   p.trace = trace;
-  p.num_blocks = pool->num_blocks;
-  p.num_kv_heads = pool->num_kv_heads;
-  p.num_q_heads = num_q_heads;
-  p.batch = batch;
-  p.bt_stride = bt_stride;
-  p.max_ctx = max_context_len;
   p.part_tokens = pl.part_tokens;
   p.num_parts = pl.num_parts;
+  p.token_offset = 0;
+  p.part_offset = 0;
+  p.part_stride = pl.num_parts;
+  p.write_partials = split ? 1 : 0;
   p.trace_tiles = trace_tiles;
-  p.scale_log2 = scale * 1.4426950408889634f;
-  // GQA groups of 8 at head_dim 128 form dense 16x16 tiles: matrix cores;
-  // everything else runs on VALU dot products.
-  hipError_t e = (group == 8 && pool->head_dim == 128)
-                     ? pa::launch_decode_mfma(p, tracing, static_cast<hipStream_t>(stream))
-                     : pa::launch_decode_valu(p, pool->head_dim, group, tracing,
-                                              static_cast<hipStream_t>(stream));
+  hipError_t e = launch_decode(p, a.pool, group, tracing, stream);
   if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
+  return PA_OK;
+}
+
+// Partition plan of a shared-prefix (cascade) step.
+struct CascadePlan {
+  int32_t pre_parts, pre_tokens;  // prefix partitions and their size
+  int32_t suf_parts, suf_tokens;  // partitions of the rest of the longest context
+  int32_t stride;                 // partitions per (sequence, head)
+};
+
+int plan_cascade(int32_t max_context_len, int32_t partition_size, int32_t prefix_len,
+                 int32_t prefix_partition_size, CascadePlan* out, const char* fn) {
+  if (max_context_len < 0) return fail(PA_EINVAL, "%s: max_context_len = %d < 0", fn, max_context_len);
+  if (partition_size <= 0 || partition_size % PA_BLOCK_SIZE != 0)
+    return fail(PA_EINVAL, "%s: partition_size = %d is not a positive multiple of %d", fn,
+                partition_size, PA_BLOCK_SIZE);
+  if (prefix_len < 0 || prefix_len % PA_BLOCK_SIZE != 0)
+    return fail(PA_EINVAL, "%s: prefix_len = %d is not a non-negative multiple of %d", fn,
+                prefix_len, PA_BLOCK_SIZE);
+  if (prefix_len > max_context_len)
+    return fail(PA_EINVAL, "%s: prefix_len = %d exceeds max_context_len = %d", fn, prefix_len,
+                max_context_len);
+  if (prefix_partition_size < PA_BLOCK_SIZE || prefix_partition_size > 64 * PA_BLOCK_SIZE ||
+      prefix_partition_size % PA_BLOCK_SIZE != 0)
+    return fail(PA_EINVAL, "%s: prefix_partition_size = %d not a multiple of 16 in [16, 1024]", fn,
+                prefix_partition_size);
+  out->pre_tokens = prefix_partition_size;
+  out->pre_parts = (prefix_len + prefix_partition_size - 1) / prefix_partition_size;
+  out->suf_tokens = partition_size;
+  const int64_t rest = (int64_t)max_context_len - prefix_len;
+  out->suf_parts = (int32_t)((rest + partition_size - 1) / partition_size);
+  const int64_t stride = (int64_t)out->pre_parts + out->suf_parts;
+  out->stride = (int32_t)(stride > 0 ? stride : 1);
   return PA_OK;
 }
 
@@ -314,9 +381,10 @@ int paged_attn_decode(const pa_kv_pool* pool, const void* q, const int32_t* bloc
                       int32_t num_q_heads, float scale, int32_t max_context_len,
                       int32_t partition_size, void* out, float* partial_out, float* partial_lse,
                       void* stream) {
-  return decode_impl(pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
-                     max_context_len, partition_size, out, partial_out, partial_lse, nullptr, 0,
-                     false, stream, "paged_attn_decode");
+  const DecodeArgs a{pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
+                     max_context_len};
+  return decode_impl(a, partition_size, out, partial_out, partial_lse, nullptr, 0, false, stream,
+                     "paged_attn_decode");
 }
 
 int paged_attn_decode_trace(const pa_kv_pool* pool, const void* q, const int32_t* block_tables,
@@ -325,16 +393,102 @@ int paged_attn_decode_trace(const pa_kv_pool* pool, const void* q, const int32_t
                             int32_t partition_size, void* out, float* partial_out,
                             float* partial_lse, int32_t* trace, int64_t trace_capacity,
                             void* stream) {
-  return decode_impl(pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
-                     max_context_len, partition_size, out, partial_out, partial_lse, trace,
-                     trace_capacity, true, stream, "paged_attn_decode_trace");
+  const DecodeArgs a{pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
+                     max_context_len};
+  return decode_impl(a, partition_size, out, partial_out, partial_lse, trace, trace_capacity, true,
+                     stream, "paged_attn_decode_trace");
 }
 
-int paged_attn_reduce(const float* partial_out, const float* partial_lse,
-                      const int32_t* context_lens, int32_t batch, int32_t num_q_heads,
-                      int32_t head_dim, int32_t partition_size, int32_t max_partitions, void* out,
-                      void* stream) {
-  const char* fn = "paged_attn_reduce";
+int paged_attn_cascade_workspace_size(int32_t batch, int32_t num_q_heads, int32_t head_dim,
+                                      int32_t max_context_len, int32_t partition_size,
+                                      int32_t prefix_len, int32_t prefix_partition_size,
+                                      size_t* partial_out_bytes, size_t* partial_lse_bytes,
+                                      int32_t* max_partitions_out) {
+  const char* fn = "paged_attn_cascade_workspace_size";
+  if (!partial_out_bytes || !partial_lse_bytes || !max_partitions_out)
+    return fail(PA_EINVAL, "%s: NULL output pointer", fn);
+  if (batch < 0 || num_q_heads <= 0 || head_dim <= 0) return fail(PA_EINVAL, "%s: bad geometry", fn);
+  CascadePlan cp;
+  int rc = plan_cascade(max_context_len, partition_size, prefix_len, prefix_partition_size, &cp, fn);
+  if (rc) return rc;
+  const size_t rows = (size_t)batch * num_q_heads * cp.stride;
+  *partial_out_bytes = rows * head_dim * sizeof(float);
+  *partial_lse_bytes = rows * sizeof(float);
+  *max_partitions_out = cp.stride;
+  return PA_OK;
+}
+
+int paged_attn_decode_cascade(const pa_kv_pool* pool, const void* q, const int32_t* block_tables,
+                              int32_t bt_stride, const int32_t* context_lens, int32_t batch,
+                              int32_t num_q_heads, float scale, int32_t max_context_len,
+                              int32_t partition_size, int32_t prefix_len,
+                              int32_t prefix_partition_size, float* partial_out,
+                              float* partial_lse, void* stream) {
+  const char* fn = "paged_attn_decode_cascade";
+  const DecodeArgs a{pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
+                     max_context_len};
+  int32_t group = 0;
+  int rc = validate_decode(a, &group, fn);
+  if (rc) return rc;
+  CascadePlan cp;
+  rc = plan_cascade(max_context_len, partition_size, prefix_len, prefix_partition_size, &cp, fn);
+  if (rc) return rc;
+  if (prefix_len > 0 && pool->head_dim != 128)
+    return fail(PA_EUNSUPPORTED, "%s: the shared-prefix pass needs head_dim 128", fn);
+  const int64_t rows = (int64_t)batch * num_q_heads;
+  const int64_t g_pre = (int64_t)cp.pre_parts * ((rows / pool->num_kv_heads + 63) / 64) * pool->num_kv_heads;
+  const int64_t g_suf = (int64_t)cp.suf_parts * batch * pool->num_kv_heads;
+  if (g_pre > 0x7fffffffLL || g_suf > 0x7fffffffLL)
+    return fail(PA_EINVAL, "%s: grid too large", fn);
+  if (batch == 0) return PA_OK;
+  if (!partial_out || !partial_lse) return fail(PA_EINVAL, "%s: partial buffers are NULL", fn);
+  if (!aligned(partial_out, 16) || !aligned(partial_lse, 4))
+    return fail(PA_EINVAL, "%s: partial buffers are misaligned", fn);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (cp.pre_parts > 0) {
+    pa::PrefixParams pp{};
+    pp.k_pool = pool->k;
+    pp.v_pool = pool->v;
+    pp.q = static_cast<const uint16_t*>(q);
+    pp.block_tables = block_tables;
+    pp.context_lens = context_lens;
+    pp.part_o = partial_out;
+    pp.part_lse = partial_lse;
+    pp.num_blocks = pool->num_blocks;
+    pp.num_kv_heads = pool->num_kv_heads;
+    pp.num_q_heads = num_q_heads;
+    pp.batch = batch;
+    pp.prefix_len = prefix_len;
+    pp.part_tokens = cp.pre_tokens;
+    pp.prefix_parts = cp.pre_parts;
+    pp.part_stride = cp.stride;
+    pp.max_ctx = max_context_len;
+    pp.scale_log2 = scale * 1.4426950408889634f;
+    hipError_t e = pa::launch_prefix_mfma(pp, group, st);
+    if (e != hipSuccess) return fail(PA_EHIP, "%s: prefix kernel launch failed: %s", fn, hipGetErrorString(e));
+  }
+  if (cp.suf_parts > 0) {
+    pa::DecodeParams p = decode_params(a);
+    p.part_o = partial_out;
+    p.part_lse = partial_lse;
+    p.part_tokens = cp.suf_tokens;
+    p.num_parts = cp.suf_parts;
+    p.token_offset = prefix_len;
+    p.part_offset = cp.pre_parts;
+    p.part_stride = cp.stride;
+    p.write_partials = 1;
+    p.trace_tiles = cp.suf_tokens / PA_BLOCK_SIZE;
+    hipError_t e = launch_decode(p, pool, group, false, stream);
+    if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
+  }
+  return PA_OK;
+}
+
+namespace {
+int reduce_impl(const float* partial_out, const float* partial_lse, const int32_t* context_lens,
+                int32_t batch, int32_t num_q_heads, int32_t head_dim, int32_t partition_size,
+                int32_t max_partitions, int32_t prefix_parts, int32_t prefix_len, void* out,
+                void* stream, const char* fn) {
   if (batch < 0) return fail(PA_EINVAL, "%s: batch = %d < 0", fn, batch);
   if (num_q_heads <= 0) return fail(PA_EINVAL, "%s: num_q_heads = %d <= 0", fn, num_q_heads);
   if (head_dim != 64 && head_dim != 128)
@@ -343,6 +497,9 @@ int paged_attn_reduce(const float* partial_out, const float* partial_lse,
     return fail(PA_EINVAL, "%s: partition_size = %d is not a positive multiple of %d", fn,
                 partition_size, PA_BLOCK_SIZE);
   if (max_partitions <= 0) return fail(PA_EINVAL, "%s: max_partitions = %d <= 0", fn, max_partitions);
+  if (prefix_parts > max_partitions)
+    return fail(PA_EINVAL, "%s: %d prefix partitions exceed max_partitions = %d", fn, prefix_parts,
+                max_partitions);
   if ((int64_t)batch * num_q_heads > 0x7fffffffLL) return fail(PA_EINVAL, "%s: grid too large", fn);
   if (batch == 0) return PA_OK;
   if (!partial_out || !partial_lse || !context_lens || !out)
@@ -358,10 +515,39 @@ int paged_attn_reduce(const float* partial_out, const float* partial_lse,
   p.batch = batch;
   p.num_q_heads = num_q_heads;
   p.part_tokens = partition_size;
-  p.num_parts = max_partitions;
+  p.part_stride = max_partitions;
+  p.prefix_parts = prefix_parts;
+  p.prefix_len = prefix_len;
   hipError_t e = pa::launch_reduce(p, head_dim, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
   return PA_OK;
+}
+}  // namespace
+
+int paged_attn_reduce(const float* partial_out, const float* partial_lse,
+                      const int32_t* context_lens, int32_t batch, int32_t num_q_heads,
+                      int32_t head_dim, int32_t partition_size, int32_t max_partitions, void* out,
+                      void* stream) {
+  return reduce_impl(partial_out, partial_lse, context_lens, batch, num_q_heads, head_dim,
+                     partition_size, max_partitions, 0, 0, out, stream, "paged_attn_reduce");
+}
+
+int paged_attn_reduce_cascade(const float* partial_out, const float* partial_lse,
+                              const int32_t* context_lens, int32_t batch, int32_t num_q_heads,
+                              int32_t head_dim, int32_t partition_size, int32_t prefix_len,
+                              int32_t prefix_partition_size, int32_t max_partitions, void* out,
+                              void* stream) {
+  const char* fn = "paged_attn_reduce_cascade";
+  if (prefix_len < 0 || prefix_len % PA_BLOCK_SIZE != 0)
+    return fail(PA_EINVAL, "%s: prefix_len = %d is not a non-negative multiple of %d", fn,
+                prefix_len, PA_BLOCK_SIZE);
+  if (prefix_partition_size < PA_BLOCK_SIZE || prefix_partition_size > 64 * PA_BLOCK_SIZE ||
+      prefix_partition_size % PA_BLOCK_SIZE != 0)
+    return fail(PA_EINVAL, "%s: prefix_partition_size = %d not a multiple of 16 in [16, 1024]", fn,
+                prefix_partition_size);
+  const int32_t pre_parts = (prefix_len + prefix_partition_size - 1) / prefix_partition_size;
+  return reduce_impl(partial_out, partial_lse, context_lens, batch, num_q_heads, head_dim,
+                     partition_size, max_partitions, pre_parts, prefix_len, out, stream, fn);
 }
 
 int pa_stream_copy(const void* src, void* dst, size_t bytes, void* stream) {

@@ -24,9 +24,35 @@ struct DecodeParams {
   int32_t bt_stride;
   int32_t max_ctx;
   int32_t part_tokens;           // tokens per work item (a multiple of 16)
-  int32_t num_parts;             // partitions in the grid (1 = no split)
+  int32_t num_parts;             // partitions in the grid
+  int32_t token_offset;          // first token of partition 0 (a multiple of 16)
+  int32_t part_offset;           // index of partition 0 in the partial buffers
+  int32_t part_stride;           // partitions per (sequence, head) in the partial buffers
+  int32_t write_partials;        // 1: write (o, lse) partials; 0: write the bf16 output
   int32_t trace_tiles;           // trace slots per work item
   float scale_log2;              // softmax scale * log2(e)
+};
+
+// Attention of every query row of the batch over a prefix that all
+// sequences share (same physical blocks, read from sequence 0's table).
+struct PrefixParams {
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const uint16_t* q;
+  const int32_t* block_tables;   // only row 0 is read
+  const int32_t* context_lens;
+  float* part_o;                 // partitions [0, prefix_parts) of the partial buffers
+  float* part_lse;
+  int32_t num_blocks;
+  int32_t num_kv_heads;
+  int32_t num_q_heads;
+  int32_t batch;
+  int32_t prefix_len;            // shared tokens (a multiple of 16)
+  int32_t part_tokens;           // tokens per prefix partition (a multiple of 16)
+  int32_t prefix_parts;          // ceil(prefix_len / part_tokens)
+  int32_t part_stride;
+  int32_t max_ctx;
+  float scale_log2;
 };
 
 struct ReduceParams {
@@ -36,8 +62,10 @@ struct ReduceParams {
   uint16_t* out;
   int32_t batch;
   int32_t num_q_heads;
-  int32_t part_tokens;
-  int32_t num_parts;
+  int32_t part_tokens;           // suffix partition size
+  int32_t part_stride;           // partitions per (sequence, head) in the buffers
+  int32_t prefix_parts;          // leading partitions that every sequence has
+  int32_t prefix_len;            // tokens covered by those partitions
 };
 
 // VALU split-KV decode (group size 4 or 8, head_dim 64 or 128).
@@ -45,6 +73,8 @@ hipError_t launch_decode_valu(const DecodeParams& p, int head_dim, int group, bo
                               hipStream_t stream);
 // MFMA split-KV decode for group size 8, head_dim 128.
 hipError_t launch_decode_mfma(const DecodeParams& p, bool trace, hipStream_t stream);
+// MFMA attention over a prefix shared by the whole batch (group 4 or 8, D 128).
+hipError_t launch_prefix_mfma(const PrefixParams& p, int group, hipStream_t stream);
 // Log-sum-exp merge of split-KV partials into the bf16 output.
 hipError_t launch_reduce(const ReduceParams& p, int head_dim, hipStream_t stream);
 // Streaming device copy (measurement helper).

@@ -37,6 +37,10 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
 // 2^x on the hardware transcendental unit (v_exp_f32); exp2(-inf) = 0.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Fourth word of a raw buffer descriptor on gfx9-family GPUs (32-bit data
+// format, no swizzle); the first three hold the base and the byte size.
+constexpr int kBufferDescWord3 = 0x00020000;
+
 // ---- cross-lane movement ---------------------------------------------------
 
 // DPP controls (gfx9 encoding).
@@ -55,6 +59,43 @@ __device__ __forceinline__ float dpp(float x) {
 template <int T>
 __device__ __forceinline__ float row_bcast(float x) {
   return dpp<kDppRowNewBcast + T>(x);
+}
+
+constexpr int kDppRowHalfMirror = 0x141;  // lane i <-> 7 - i within each half-row of 8
+
+// Max / sum over the 4 lanes of each quad; every lane receives the result.
+__device__ __forceinline__ float quad_max4(float x) {
+  x = fmaxf(x, dpp<kDppQuadXor1>(x));
+  return fmaxf(x, dpp<kDppQuadXor2>(x));
+}
+__device__ __forceinline__ float quad_sum4(float x) {
+  x += dpp<kDppQuadXor1>(x);
+  return x + dpp<kDppQuadXor2>(x);
+}
+
+// One level of a reduce-scatter: each lane pairs with the lane CTRL maps it
+// to; the lane with `upper` set keeps the upper half of x[0..2H) and the other
+// the lower half, each adding its partner's copy of the half it keeps.
+template <int CTRL, int H, int N>
+__device__ __forceinline__ void reduce_scatter_level(float (&x)[N], bool upper) {
+#pragma unroll
+  for (int i = 0; i < H; ++i) {
+    const float send = upper ? x[i] : x[i + H];
+    const float keep = upper ? x[i + H] : x[i];
+    x[i] = keep + dpp<CTRL>(send);
+  }
+}
+
+// Reduce-scatter over the 16 lanes of each DPP row.  Every lane holds N
+// partial values (N a multiple of 16); afterwards lane c of a row holds in
+// x[0 .. N/16) the row-wide sums of values c*N/16 .. c*N/16 + N/16 - 1.
+template <int N>
+__device__ __forceinline__ void row_reduce_scatter16(float (&x)[N], int c) {
+  static_assert(N % 16 == 0, "N must be a multiple of 16");
+  reduce_scatter_level<kDppRowRor8, N / 2>(x, (c & 8) != 0);        // partner c ^ 8
+  reduce_scatter_level<kDppRowHalfMirror, N / 4>(x, (c & 4) != 0);  // partner (c & 8) | (7 - c % 8)
+  reduce_scatter_level<kDppQuadXor2, N / 8>(x, (c & 2) != 0);       // partner c ^ 2
+  reduce_scatter_level<kDppQuadXor1, N / 16>(x, (c & 1) != 0);      // partner c ^ 1
 }
 
 // Max / sum over the 16 lanes of each row; every lane receives the result.
@@ -107,6 +148,24 @@ __device__ __forceinline__ void allgather4(float x, float& r0, float& r1, float&
   swap16(a, c);        // a: x_0, c: x_1
   swap16(b, d);        // b: x_2, d: x_3
   r0 = a; r1 = c; r2 = b; r3 = d;
+}
+
+// All-reduce over the four 16-lane groups (lanes i, i+16, i+32, i+48).
+__device__ __forceinline__ float group_max4(float x) {
+  float a = x, b = x;
+  swap32(a, b);
+  const float y = fmaxf(a, b);
+  float c = y, d = y;
+  swap16(c, d);
+  return fmaxf(c, d);
+}
+__device__ __forceinline__ float group_sum4(float x) {
+  float a = x, b = x;
+  swap32(a, b);
+  const float y = a + b;
+  float c = y, d = y;
+  swap16(c, d);
+  return c + d;
 }
 
 __device__ __forceinline__ int wave_uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }

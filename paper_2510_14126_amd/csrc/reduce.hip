@@ -1,8 +1,9 @@
 // Cross-split reduce: merge split-KV partials into the bf16 output.
 //
-// For sequence b and query head h the decode kernel left, per partition p,
+// For sequence b and query head h the decode kernels left, per partition p,
 // the partition-normalised output o_p and its log-sum-exp lse_p (natural
-// log).  With P_b = ceil(ctx_b / S) partitions and M = max_p lse_p:
+// log): first the partitions of a prefix shared by the whole batch (if any),
+// then ceil((ctx_b - prefix) / S) partitions of the rest.  With M = max lse_p:
 //     w_p = exp(lse_p - M),   out = sum_p w_p o_p / sum_p w_p,
 // which is exactly softmax attention over the whole context.  One wavefront
 // per (b, h); lane l owns dims (D/64)*l ..; partitions are summed in order,
@@ -19,12 +20,12 @@ __global__ void __launch_bounds__(64) reduce_kernel(const ReduceParams p) {
   const int lane = threadIdx.x;
   const int bh = blockIdx.x;
   const int b = bh / p.num_q_heads;
-  int n = p.context_lens[b];
+  int n = p.context_lens[b] - p.prefix_len;
   n = n < 0 ? 0 : n;
-  int pb = n / p.part_tokens + (n % p.part_tokens != 0);
-  pb = pb > p.num_parts ? p.num_parts : pb;
-  const float* lse = p.part_lse + (size_t)bh * p.num_parts;
-  const float* po = p.part_o + (size_t)bh * p.num_parts * D + DPL * lane;
+  int pb = p.prefix_parts + n / p.part_tokens + (n % p.part_tokens != 0);
+  pb = pb > p.part_stride ? p.part_stride : pb;
+  const float* lse = p.part_lse + (size_t)bh * p.part_stride;
+  const float* po = p.part_o + (size_t)bh * p.part_stride * D + DPL * lane;
 
   float mx = -__builtin_inff();
   for (int q = 0; q < pb; ++q) mx = fmaxf(mx, lse[q]);

@@ -23,7 +23,8 @@ def _dev(a: np.ndarray, device) -> torch.Tensor:
 
 class PagedBatch:
     def __init__(self, w, device="cuda:0", partition_size: int | None = None,
-                 register_blocks: bool = True, k_pool=None, v_pool=None):
+                 register_blocks: bool = True, k_pool=None, v_pool=None,
+                 prefix_len: int = 0, prefix_partition_size: int = 256):
         self.w = w
         self.device = torch.device(device)
         self.partition_size = w.partition_size if partition_size is None else partition_size
@@ -39,9 +40,16 @@ class PagedBatch:
                                            w.head_dim, self.k, self.v)
         if register_blocks:
             self.register_placement()
-        self.num_parts = binding.paged_attn_num_partitions(self.max_ctx, self.partition_size)
-        ob, lb = binding.paged_attn_workspace_size(self.batch, self.hq, self.d, self.max_ctx,
-                                                   self.partition_size)
+        self.prefix_len = prefix_len
+        self.prefix_partition_size = prefix_partition_size
+        if prefix_len:
+            ob, lb, self.num_parts = binding.paged_attn_cascade_workspace_size(
+                self.batch, self.hq, self.d, self.max_ctx, self.partition_size, prefix_len,
+                prefix_partition_size)
+        else:
+            self.num_parts = binding.paged_attn_num_partitions(self.max_ctx, self.partition_size)
+            ob, lb = binding.paged_attn_workspace_size(self.batch, self.hq, self.d, self.max_ctx,
+                                                       self.partition_size)
         self.part_o = torch.empty(ob // 4, dtype=torch.float32, device=self.device) if ob else None
         self.part_lse = torch.empty(lb // 4, dtype=torch.float32, device=self.device) if lb else None
 
@@ -62,20 +70,36 @@ class PagedBatch:
         return int(self.w.block_tables.shape[1])
 
     def decode(self, stream=None, out=None) -> None:
+        if self.prefix_len:
+            binding.paged_attn_decode_cascade(
+                self.pool, self.q, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,
+                self.w.scale, self.max_ctx, self.partition_size, self.prefix_len,
+                self.prefix_partition_size, self.part_o, self.part_lse, stream)
+            return
         binding.paged_attn_decode(self.pool, self.q, self.bt, self.bt_stride, self.ctx, self.batch,
                                   self.hq, self.w.scale, self.max_ctx, self.partition_size,
                                   self.out if out is None else out, self.part_o, self.part_lse,
                                   stream)
 
     def reduce(self, stream=None, out=None) -> None:
+        if self.prefix_len:
+            binding.paged_attn_reduce_cascade(
+                self.part_o, self.part_lse, self.ctx, self.batch, self.hq, self.d,
+                self.partition_size, self.prefix_len, self.prefix_partition_size, self.num_parts,
+                self.out if out is None else out, stream)
+            return
         binding.paged_attn_reduce(self.part_o, self.part_lse, self.ctx, self.batch, self.hq, self.d,
                                   self.partition_size, self.num_parts,
                                   self.out if out is None else out, stream)
 
+    @property
+    def needs_reduce(self) -> bool:
+        return bool(self.prefix_len) or self.num_parts > 1
+
     def run(self, stream=None) -> None:
-        """One decode step: split-KV decode, then the merge when it split."""
+        """One decode step: split-KV (or cascade) decode, then the merge."""
         self.decode(stream)
-        if self.num_parts > 1:
+        if self.needs_reduce:
             self.reduce(stream)
 
     def out_bits(self) -> np.ndarray:

@@ -46,6 +46,8 @@ def run(w, S=None, **kw):
 
 def gpu_out(w, S=None, **kw):
     pb = run(w, S, **kw)
+    if pb.needs_reduce and not pb.prefix_len and pb.num_parts == 1:
+        raise AssertionError("inconsistent reduce plan")
     out = pb.out_bits()
     pb.close()
     return out
@@ -391,3 +393,95 @@ def test_growing_scores_force_rescales(S, hq):
     ref, lse = decode_workload(w)
     assert np.ptp(lse) > 10
     assert_gate(gpu_out(w, S), ref, f"growing scores S={S} Hq={hq}")
+
+
+# ------------------------------------------------- shared-prefix cascade
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_cascade_stage_configs_all_outputs(k):
+    w = build_config(k)
+    L = w.meta["prefix_blocks"] * 16
+    say(f"cascade config {k} {w.name}: prefix {L}")
+    out = gpu_out(w, prefix_len=L, prefix_partition_size=256)
+    assert_gate(out, decode_workload(w)[0], f"cascade config {k}")
+
+
+def test_cascade_long_context_sampled():
+    say("cascade config 5 build")
+    w = build_config(5)
+    L = w.meta["prefix_blocks"] * 16
+    out = gpu_out(w, prefix_len=L, prefix_partition_size=512)
+    seqs = [0, int(np.argmax(w.context_lens)), int(np.argmin(w.context_lens)), 77]
+    assert_gate(out[seqs], decode_workload(w, seqs=seqs)[0], "cascade config 5 sampled")
+
+
+CASCADE_CASES = [
+    # seed, B, Hq, Hkv, ctx, prefix, S, S_pre
+    (70, 5, 32, 8, [300, 47, 1000, 64, 129], 32, 512, 16),
+    (71, 6, 32, 8, [512, 512, 600, 1100, 513, 700], 512, 64, 256),
+    (72, 3, 64, 8, [2100, 2048, 4000], 2048, 512, 1024),
+    (73, 17, 32, 8, list(range(240, 240 + 17 * 13, 13)), 224, 512, 128),
+    (74, 9, 16, 2, [100 + 37 * i for i in range(9)], 96, 128, 32),
+    (75, 4, 8, 1, [16, 17, 33, 80], 16, 16, 16),
+]
+
+
+@pytest.mark.parametrize("case", CASCADE_CASES, ids=[f"seed{c[0]}" for c in CASCADE_CASES])
+def test_cascade_edge_shapes(case):
+    seed, B, hq, hkv, ctx, pre, S, Spre = case
+    say(f"cascade edges seed={seed} B={B} Hq={hq} Hkv={hkv} prefix={pre} S={S} S_pre={Spre}")
+    lc = logical_case(seed, B, hq, hkv, 128, ctx, prefix_len=pre)
+    w = page_case(lc, seed + 1, extra_blocks=4)
+    ref = decode_workload(w)[0]
+    out = gpu_out(w, S, prefix_len=pre, prefix_partition_size=Spre)
+    assert_gate(out, ref, f"cascade seed {seed}")
+    # same result as the per-sequence path up to rounding
+    plain = gpu_out(w, S)
+    assert compare(out, bf16_to_f64(plain), gpu_is_bf16_bits=True).passed
+
+
+def test_cascade_sequence_shorter_than_prefix():
+    say("cascade with a sequence shorter than the prefix")
+    lc = logical_case(80, 4, 32, 8, 128, [700, 520, 900, 512], prefix_len=512)
+    w = page_case(lc, 81)
+    w.context_lens = w.context_lens.copy()
+    w.context_lens[1] = 492          # attends only to the first 492 prefix tokens
+    w.context_lens[3] = 0            # empty
+    ref = decode_workload(w)[0]
+    out = gpu_out(w, 512, prefix_len=512, prefix_partition_size=128)
+    assert np.all(out[3] & 0x7FFF == 0)
+    assert_gate(out, ref, "cascade short sequence")
+
+
+@pytest.mark.parametrize("where", ["prefix", "suffix"])
+@pytest.mark.parametrize("hq", [32, 64])
+def test_cascade_argmax_exact_slot(hq, where):
+    """One dominant token -- in the shared prefix (every sequence must select
+    the same slot) or in each sequence's own suffix -- is selected exactly;
+    rows past the context and unused blocks are poisoned."""
+    say(f"cascade argmax Hq={hq} target in {where}")
+    ctx = [600, 700, 530, 1000]
+    lc = logical_case(90, 4, hq, 8, 128, ctx, prefix_len=512)
+    w = page_case(lc, 91, extra_blocks=6, poison=True)
+    e0 = np.zeros(128, np.float32); e0[0] = 1.0
+    w.q[:] = f32_to_bf16_bits(e0)
+    nblk = (w.context_lens + 15) // 16
+    for b in range(4):
+        for j in range(nblk[b]):
+            pid = int(w.block_tables[b, j])
+            for r in range(min(16, int(w.context_lens[b]) - 16 * j)):
+                w.k_pool[pid, :, r, :] = 0
+                w.v_pool[pid, :, r, :] = 0
+                w.v_pool[pid, :, r, 0:3] = f32_to_bf16_bits(np.float32([pid % 256, pid // 256, r]))
+    targets = [300] * 4 if where == "prefix" else [599, 512, 529, 999]
+    want = []
+    for b, t in enumerate(targets):
+        pid = int(w.block_tables[b, t // 16])
+        w.k_pool[pid, :, t % 16, 0] = 0x4580   # 4096.0
+        want.append((pid, t % 16))
+    out = gpu_out(w, 512, prefix_len=512, prefix_partition_size=128)
+    for b, (pid, r) in enumerate(want):
+        got = bf16_to_f64(out[b, :, :3])
+        assert np.all(got[:, 0] == pid % 256) and np.all(got[:, 1] == pid // 256) \
+            and np.all(got[:, 2] == r), f"seq {b}: wanted slot ({pid},{r}), got {got[0]}"
+        assert np.all(out[b, :, 3:] & 0x7FFF == 0)
