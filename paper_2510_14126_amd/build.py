@@ -15,7 +15,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB_PATH = os.path.join(HERE, "libpaged_attn.so")
-SOURCES = ["api.cpp", "decode_valu.hip", "decode_mfma.hip", "reduce.hip", "stream_copy.hip"]
+SOURCES = ["api.cpp", "decode_valu.hip", "decode_mfma.hip", "cascade.hip", "reduce.hip",
+           "stream_copy.hip"]
 ARCH = "gfx950"
 
 COMMON_FLAGS = [

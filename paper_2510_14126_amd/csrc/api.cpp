@@ -436,48 +436,52 @@ int paged_attn_decode_cascade(const pa_kv_pool* pool, const void* q, const int32
   if (prefix_len > 0 && pool->head_dim != 128)
     return fail(PA_EUNSUPPORTED, "%s: the shared-prefix pass needs head_dim 128", fn);
   const int64_t rows = (int64_t)batch * num_q_heads;
-  const int64_t g_pre = (int64_t)cp.pre_parts * ((rows / pool->num_kv_heads + 63) / 64) * pool->num_kv_heads;
+  // Upper bound on the fused grid: a prefix workgroup covers at least 16 query
+  // rows of one KV head, a suffix workgroup one (sequence, KV head) pair.
+  const int64_t g_pre = (int64_t)cp.pre_parts * ((rows / pool->num_kv_heads + 15) / 16) * pool->num_kv_heads;
   const int64_t g_suf = (int64_t)cp.suf_parts * batch * pool->num_kv_heads;
-  if (g_pre > 0x7fffffffLL || g_suf > 0x7fffffffLL)
+  if (g_pre + g_suf > 0x7fffffffLL)
     return fail(PA_EINVAL, "%s: grid too large", fn);
   if (batch == 0) return PA_OK;
   if (!partial_out || !partial_lse) return fail(PA_EINVAL, "%s: partial buffers are NULL", fn);
   if (!aligned(partial_out, 16) || !aligned(partial_lse, 4))
     return fail(PA_EINVAL, "%s: partial buffers are misaligned", fn);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (cp.pre_parts > 0) {
-    pa::PrefixParams pp{};
-    pp.k_pool = pool->k;
-    pp.v_pool = pool->v;
-    pp.q = static_cast<const uint16_t*>(q);
-    pp.block_tables = block_tables;
-    pp.context_lens = context_lens;
-    pp.part_o = partial_out;
-    pp.part_lse = partial_lse;
-    pp.num_blocks = pool->num_blocks;
-    pp.num_kv_heads = pool->num_kv_heads;
-    pp.num_q_heads = num_q_heads;
-    pp.batch = batch;
-    pp.prefix_len = prefix_len;
-    pp.part_tokens = cp.pre_tokens;
-    pp.prefix_parts = cp.pre_parts;
-    pp.part_stride = cp.stride;
-    pp.max_ctx = max_context_len;
-    pp.scale_log2 = scale * 1.4426950408889634f;
-    hipError_t e = pa::launch_prefix_mfma(pp, group, st);
-    if (e != hipSuccess) return fail(PA_EHIP, "%s: prefix kernel launch failed: %s", fn, hipGetErrorString(e));
+  pa::PrefixParams pp{};
+  pp.k_pool = pool->k;
+  pp.v_pool = pool->v;
+  pp.q = static_cast<const uint16_t*>(q);
+  pp.block_tables = block_tables;
+  pp.context_lens = context_lens;
+  pp.part_o = partial_out;
+  pp.part_lse = partial_lse;
+  pp.num_blocks = pool->num_blocks;
+  pp.num_kv_heads = pool->num_kv_heads;
+  pp.num_q_heads = num_q_heads;
+  pp.batch = batch;
+  pp.prefix_len = prefix_len;
+  pp.part_tokens = cp.pre_tokens;
+  pp.prefix_parts = cp.pre_parts;
+  pp.part_stride = cp.stride;
+  pp.max_ctx = max_context_len;
+  pp.scale_log2 = scale * 1.4426950408889634f;
+  pa::DecodeParams p = decode_params(a);
+  p.part_o = partial_out;
+  p.part_lse = partial_lse;
+  p.part_tokens = cp.suf_tokens;
+  p.num_parts = cp.suf_parts;
+  p.token_offset = prefix_len;
+  p.part_offset = cp.pre_parts;
+  p.part_stride = cp.stride;
+  p.write_partials = 1;
+  p.trace_tiles = cp.suf_tokens / PA_BLOCK_SIZE;
+  if (pool->head_dim == 128) {
+    // prefix pass and per-sequence decode in one grid
+    hipError_t e = pa::launch_cascade(pp, p, group, st);
+    if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
+    return PA_OK;
   }
-  if (cp.suf_parts > 0) {
-    pa::DecodeParams p = decode_params(a);
-    p.part_o = partial_out;
-    p.part_lse = partial_lse;
-    p.part_tokens = cp.suf_tokens;
-    p.num_parts = cp.suf_parts;
-    p.token_offset = prefix_len;
-    p.part_offset = cp.pre_parts;
-    p.part_stride = cp.stride;
-    p.write_partials = 1;
-    p.trace_tiles = cp.suf_tokens / PA_BLOCK_SIZE;
+  if (cp.suf_parts > 0) {  // no prefix (head_dim 64 requires prefix_len 0)
     hipError_t e = launch_decode(p, pool, group, false, stream);
     if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
   }

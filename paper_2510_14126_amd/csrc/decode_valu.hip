@@ -1,373 +1,15 @@
-// Split-KV paged decode attention on VALU dot products (gfx950).
-//
-// One workgroup handles one work item (partition p, sequence b, KV head g):
-// the G query heads g*G .. g*G+G-1 that share KV head g attend to the
-// tokens [p*S, min((p+1)*S, ctx_b)) of sequence b.  Its W wavefronts take
-// the partition's 16-token KV blocks round-robin, each keeping its own
-// online-softmax state, and merge through LDS at the end.  Each wavefront
-// keeps NBUF tiles in a register ring, so the next NBUF-1 blocks stream in
-// while one is being computed.
-//
-// A 16-token block of one KV head is a K tile and a V tile (16 x D bf16,
-// contiguous in the pool).  Both are read in "quad lanes": lane (J, c) =
-// (lane >> 4, lane & 15) holds dims (D/16)*c .. of tokens 4u+J, u = 0..3,
-// so one 16-byte (8-byte at D = 64) load instruction reads four whole token
-// rows, contiguous in memory, and a lane needs only its (D/16)-dim slice of
-// the G query rows.
-//
-//  * QK^T: each lane forms 4G partial dot products (v_dot2c_f32_bf16) over
-//    its dims; a DPP reduce-scatter across the 16 lanes of the row (ror 8,
-//    half-mirror, quad xor 2, quad xor 1) leaves in lane (J, c) the score of
-//    query row c/4 (+4k) for token 4(c%4)+J.
-//  * PV: lane (J, c) accumulates its dims over tokens = J mod 4; the
-//    probability of token 4u+J for row r sits in the same row group, at
-//    position 4(r%4)+u, so one DPP row broadcast delivers it.  The four row
-//    groups are summed once, at the end.
-//
-// The online softmax runs in log2 units (scores times scale*log2 e, hardware
-// exp2) and rescales the accumulator only when a block raises a row max by
-// more than kLazyRescale, so probabilities stay <= 2^8 and the rescale branch
-// is wave-uniform and rare.  Tail rows are removed by select (score -inf, V
-// zero), so stale or NaN data past the context never reaches the result.
-#include "kernels.h"
-#include "pa_device.h"
-
-#include <type_traits>
-
-// Wavefronts per workgroup and tiles kept in flight per wavefront.
-#ifndef PA_VALU_WAVES
-#define PA_VALU_WAVES 4
-#endif
-#ifndef PA_VALU_NBUF
-#define PA_VALU_NBUF 3
-#endif
-#ifndef PA_VALU_MIN_WAVES
-#define PA_VALU_MIN_WAVES 2
-#endif
+// Split-KV paged decode attention on VALU dot products: kernel entry points.
+// The algorithm lives in valu_body.h.
+#include "valu_body.h"
 
 namespace pa {
 namespace {
 
-constexpr float kLazyRescale = 8.0f;
-
-template <int I, int N, typename F>
-__device__ __forceinline__ void static_for(F&& f) {
-  if constexpr (I < N) {
-    f(std::integral_constant<int, I>{});
-    static_for<I + 1, N>(f);
-  }
-}
-
-template <int D>
-struct KvTile {
-  static constexpr int VW = D / 32;   // dwords per lane per token (4: 16 B, 2: 8 B)
-  uint32_t k[4][VW];                  // token 4u + J, dims (D/16)*c ..
-  uint32_t v[4][VW];
-};
-
-// Rows 4u+J, dims (D/16)*c .. of one tile, through a buffer descriptor built
-// from the wave-uniform tile address (scalar registers) and the lane's fixed
-// byte offset inside a 4-token row quad: no per-tile vector address math, and
-// the descriptor bounds every access to the tile.
-// `bytes` = 0 turns the loads into no-ops that return zeros but still count
-// as issued, so every path through the prefetch ring issues the same loads.
-template <int D>
-__device__ __forceinline__ void load_rows(uint32_t (&dst)[4][D / 32], const uint16_t* tile,
-                                          uint32_t lane_off, int bytes) {
-  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(tile), 0, bytes, kBufferDescWord3);
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const int off = (int)lane_off + u * (4 * D * 2);
-    if constexpr (D == 128) {
-      const auto x = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0);
-      dst[u][0] = x[0]; dst[u][1] = x[1]; dst[u][2] = x[2]; dst[u][3] = x[3];
-    } else {
-      const auto x = __builtin_amdgcn_raw_buffer_load_b64(rsrc, off, 0, 0);
-      dst[u][0] = x[0]; dst[u][1] = x[1];
-    }
-  }
-}
-
-template <int D, int G>
-struct WaveState {
-  static constexpr int R = G / 4;     // score slots per lane: rows c/4 + 4k
-  static constexpr int DPL = D / 16;  // PV dims per lane
-  float m[R];                         // running row max, log2 units
-  float l[R];                         // this lane's share of the row sum
-  float acc[G][DPL];                  // unnormalised output over tokens = J mod 4
-};
-
-template <int D, int G, bool TAIL>
-__device__ __forceinline__ void process_tile(WaveState<D, G>& S, const KvTile<D>& T,
-                                             const uint32_t (&qv)[G][D / 32], int valid,
-                                             int grp, int c, float scale_log2) {
-  constexpr int R = G / 4;
-  constexpr int VW = D / 32;
-  constexpr int DPL = D / 16;
-
-  // Partial scores over this lane's dims, ordered so the reduce-scatter hands
-  // lane c the values (row c/4 + 4k, token quad c%4) in slot k.
-  float y[4 * G];
-#pragma unroll
-  for (int r = 0; r < G; ++r)
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      float a = 0.f;
-#pragma unroll
-      for (int w = 0; w < VW; ++w) a = dot2_bf16(qv[r][w], T.k[u][w], a);
-      y[R * (4 * (r % 4) + u) + r / 4] = a;
-    }
-  row_reduce_scatter16(y, c);
-
-  const int token = 4 * (c & 3) + grp;
-  float sc[R], bm[R];
-  bool raise = false;
-#pragma unroll
-  for (int k = 0; k < R; ++k) {
-    float s = y[k] * scale_log2;
-    if (TAIL && token >= valid) s = -__builtin_inff();
-    sc[k] = s;
-    bm[k] = group_max4(quad_max4(s));
-    raise |= bm[k] > S.m[k] + kLazyRescale;
-  }
-  if (__builtin_amdgcn_ballot_w64(raise) != 0) {
-    float alpha[R];
-#pragma unroll
-    for (int k = 0; k < R; ++k) {
-      const float mn = bm[k] > S.m[k] + kLazyRescale ? bm[k] : S.m[k];
-      alpha[k] = mn == -__builtin_inff() ? 1.f : fast_exp2(S.m[k] - mn);
-      S.l[k] *= alpha[k];
-      S.m[k] = mn;
-    }
-    static_for<0, G>([&](auto rc) {
-      constexpr int r = decltype(rc)::value;
-      const float a = row_bcast<4 * (r % 4)>(alpha[r / 4]);
-#pragma unroll
-      for (int d = 0; d < DPL; ++d) S.acc[r][d] *= a;
-    });
-  }
-
-  float pr[R];
-#pragma unroll
-  for (int k = 0; k < R; ++k) {
-    const float mref = S.m[k] == -__builtin_inff() ? 0.f : S.m[k];
-    pr[k] = fast_exp2(sc[k] - mref);
-    S.l[k] += pr[k];
-  }
-
-  // PV: step u covers tokens 4u + J; row r's probability is at position
-  // 4(r%4) + u of slot r/4 in the same row group.
-  static_for<0, 4>([&](auto uc) {
-    constexpr int u = decltype(uc)::value;
-    float v[DPL];
-#pragma unroll
-    for (int w = 0; w < VW; ++w) {
-      v[2 * w] = bf16_lo(T.v[u][w]);
-      v[2 * w + 1] = bf16_hi(T.v[u][w]);
-    }
-    if (TAIL && 4 * u + grp >= valid) {
-#pragma unroll
-      for (int d = 0; d < DPL; ++d) v[d] = 0.f;
-    }
-    static_for<0, G>([&](auto rc) {
-      constexpr int r = decltype(rc)::value;
-      const float pb = row_bcast<4 * (r % 4) + u>(pr[r / 4]);
-#pragma unroll
-      for (int d = 0; d < DPL; ++d) S.acc[r][d] = fmaf(pb, v[d], S.acc[r][d]);
-    });
-  });
-}
-
 template <int D, int G, int W, int NBUF, bool TRACE>
 __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(PA_VALU_MIN_WAVES, 8)))
 decode_valu_kernel(const DecodeParams p) {
-  constexpr int R = G / 4;
-  constexpr int DPL = D / 16;
-  static_assert(G == 4 || G == 8, "group size");
-  static_assert(D == 64 || D == 128, "head dim");
-
-  const int lane = threadIdx.x & 63;
-  const int wave = wave_uniform(threadIdx.x >> 6);
-  const int grp = lane >> 4;
-  const int tok = lane & 15;
-
-  // Work item; the KV head varies fastest so consecutive workgroups, which
-  // the dispatcher spreads over the XCDs round-robin, keep one KV head per XCD.
-  int wg = blockIdx.x;
-  const int g = wg % p.num_kv_heads;
-  wg /= p.num_kv_heads;
-  const int b = wg % p.batch;
-  const int part = wg / p.batch;
-
-  const int start = p.token_offset + part * p.part_tokens;
-  const int j0 = start >> 4;
-  const int h0 = g * G;
-  const int32_t* bt = p.block_tables + (size_t)b * p.bt_stride + j0;
-  // The first 64 block ids and the query rows are loaded before the context
-  // length arrives (j0 < bt_stride for every launched partition).
-  const int raw_first = lane < min(64, p.bt_stride - j0) ? bt[lane] : 0;
-
-  // Query slices: lane (J, c) keeps dims (D/16)*c .. of every query row.
-  uint32_t qv[G][D / 32];
-  {
-    const uint16_t* qb = p.q + ((size_t)b * p.num_q_heads + h0) * D + (D / 16) * tok;
-#pragma unroll
-    for (int r = 0; r < G; ++r) {
-      if constexpr (D == 128) {
-        const uint4 v = *reinterpret_cast<const uint4*>(qb + r * D);
-        qv[r][0] = v.x; qv[r][1] = v.y; qv[r][2] = v.z; qv[r][3] = v.w;
-      } else {
-        const uint2 v = *reinterpret_cast<const uint2*>(qb + r * D);
-        qv[r][0] = v.x; qv[r][1] = v.y;
-      }
-    }
-  }
-
-  int n = p.context_lens[b];
-  n = n < 0 ? 0 : (n > p.max_ctx ? p.max_ctx : n);
-  const bool split = p.write_partials != 0;
-  if (split && start >= n) return;  // whole workgroup; the reduce skips this partition
-  const int end = min(n, start + p.part_tokens);
-  const int nblk = end > start ? (end - start + 15) >> 4 : 0;
-
-  WaveState<D, G> S;
-#pragma unroll
-  for (int k = 0; k < R; ++k) { S.m[k] = -__builtin_inff(); S.l[k] = 0.f; }
-#pragma unroll
-  for (int r = 0; r < G; ++r)
-#pragma unroll
-    for (int d = 0; d < DPL; ++d) S.acc[r][d] = 0.f;
-
-  constexpr size_t kTileElems = 16 * D;
-  const size_t blk_stride = (size_t)p.num_kv_heads * kTileElems;
-  const uint16_t* kbase = p.k_pool + (size_t)g * kTileElems;
-  const uint16_t* vbase = p.v_pool + (size_t)g * kTileElems;
-  const size_t item = ((size_t)part * p.batch + b) * p.num_kv_heads + g;
-  const uint32_t lane_off = (uint32_t)(grp * D + (D / 16) * tok) * 2u;
-
-  for (int c0 = 0; c0 < nblk; c0 += 64) {
-    const int cn = min(64, nblk - c0);
-    const int raw = c0 == 0 ? (lane < cn ? raw_first : 0) : (lane < cn ? bt[c0 + lane] : 0);
-    const int idc = min(max(raw, 0), p.num_blocks - 1);
-
-    // Loads for blocks past the chunk are issued with an empty descriptor.
-    auto load = [&](KvTile<D>& T, int i) {
-      const bool ok = i < cn;
-      const size_t id = (size_t)__builtin_amdgcn_readlane(idc, ok ? i : 0);
-      const int bytes = ok ? 16 * D * 2 : 0;
-      load_rows<D>(T.k, kbase + id * blk_stride, lane_off, bytes);
-      load_rows<D>(T.v, vbase + id * blk_stride, lane_off, bytes);
-    };
-    auto run = [&](const KvTile<D>& T, int i) {
-      const int valid = min(16, end - (start + (c0 + i) * 16));
-      if (valid == 16)
-        process_tile<D, G, false>(S, T, qv, 16, grp, tok, p.scale_log2);
-      else
-        process_tile<D, G, true>(S, T, qv, valid, grp, tok, p.scale_log2);
-      if constexpr (TRACE) {
-        if (lane == 0) {
-          int32_t* tr = p.trace + (item * p.trace_tiles + (c0 + i)) * 3;
-          tr[0] = j0 + c0 + i;
-          tr[1] = __builtin_amdgcn_readlane(raw, i);
-          tr[2] = valid;
-        }
-      }
-    };
-
-    int i = wave;
-    if (i >= cn) continue;
-    KvTile<D> T[NBUF];
-    int ld = i;
-#pragma unroll
-    for (int s = 0; s < NBUF - 1; ++s) {
-      load(T[s], ld);
-      ld += W;
-    }
-    bool done = false;
-    while (!done) {
-#pragma unroll
-      for (int s = 0; s < NBUF; ++s) {
-        if (!done) {
-          load(T[(s + NBUF - 1) % NBUF], ld);
-          ld += W;
-          run(T[s], i);
-          i += W;
-          done = i >= cn;
-        }
-      }
-    }
-  }
-
-  // Row statistics of this wave: slot k of lane (J, c) belongs to row
-  // c/4 + 4k; every lane gathers all rows by row broadcast.
-  float Mw[G], Lw[G];
-  {
-    float lsum[R];
-#pragma unroll
-    for (int k = 0; k < R; ++k) lsum[k] = group_sum4(quad_sum4(S.l[k]));
-    static_for<0, G>([&](auto rc) {
-      constexpr int r = decltype(rc)::value;
-      Mw[r] = row_bcast<4 * (r % 4)>(S.m[r / 4]);
-      Lw[r] = row_bcast<4 * (r % 4)>(lsum[r / 4]);
-    });
-  }
-
-  // Merge waves and row groups through LDS; lane l then owns output dims
-  // (D/64)*l .. of every row.
-  constexpr int OPL = D / 64;
-  __shared__ float sm[W][G], sl[W][G];
-  __shared__ float sacc[W][4][G][D];
-  if (lane == 0) {
-#pragma unroll
-    for (int r = 0; r < G; ++r) { sm[wave][r] = Mw[r]; sl[wave][r] = Lw[r]; }
-  }
-#pragma unroll
-  for (int r = 0; r < G; ++r)
-#pragma unroll
-    for (int d = 0; d < DPL; ++d) sacc[wave][grp][r][DPL * tok + d] = S.acc[r][d];
-  __syncthreads();
-  if (wave != 0) return;
-
-#pragma unroll
-  for (int r = 0; r < G; ++r) {
-    float mx = sm[0][r];
-#pragma unroll
-    for (int w = 1; w < W; ++w) mx = fmaxf(mx, sm[w][r]);
-    const float mref = (mx == -__builtin_inff()) ? 0.f : mx;
-    float lt = 0.f, o[OPL];
-#pragma unroll
-    for (int d = 0; d < OPL; ++d) o[d] = 0.f;
-#pragma unroll
-    for (int w = 0; w < W; ++w) {
-      const float f = fast_exp2(sm[w][r] - mref);
-      lt = fmaf(sl[w][r], f, lt);
-#pragma unroll
-      for (int d = 0; d < OPL; ++d) {
-        const float part_sum = (sacc[w][0][r][OPL * lane + d] + sacc[w][1][r][OPL * lane + d]) +
-                               (sacc[w][2][r][OPL * lane + d] + sacc[w][3][r][OPL * lane + d]);
-        o[d] = fmaf(part_sum, f, o[d]);
-      }
-    }
-    const float inv = lt > 0.f ? 1.0f / lt : 0.f;
-    if (!split) {
-      uint16_t* orow = p.out + ((size_t)b * p.num_q_heads + h0 + r) * D;
-      if constexpr (OPL == 2)
-        *reinterpret_cast<uint32_t*>(orow + 2 * lane) =
-            bf16_rne(o[0] * inv) | (bf16_rne(o[1] * inv) << 16);
-      else
-        orow[lane] = (uint16_t)bf16_rne(o[0] * inv);
-    } else {
-      const size_t row = ((size_t)b * p.num_q_heads + h0 + r) * p.part_stride + p.part_offset + part;
-      float* po = p.part_o + row * D;
-      if constexpr (OPL == 2)
-        *reinterpret_cast<float2*>(po + 2 * lane) = make_float2(o[0] * inv, o[1] * inv);
-      else
-        po[lane] = o[0] * inv;
-      if (lane == 0)
-        p.part_lse[row] = lt > 0.f ? (mx + log2f(lt)) * kLn2 : -__builtin_inff();
-    }
-  }
+  __shared__ __attribute__((aligned(16))) uint8_t smem[valu::valu_lds_bytes<D, G, W>()];
+  valu::decode_valu_body<D, G, W, NBUF, TRACE>(p, blockIdx.x, (lds_u8_t*)smem);
 }
 
 template <int D, int G, bool TRACE>
@@ -382,14 +24,13 @@ hipError_t launch_t(const DecodeParams& p, hipStream_t stream) {
 
 }  // namespace
 
+// GQA groups of 8 at head_dim 128 run on matrix cores (decode_mfma.hip).
 hipError_t launch_decode_valu(const DecodeParams& p, int head_dim, int group, bool trace,
                               hipStream_t stream) {
   if (head_dim == 128 && group == 4)
     return trace ? launch_t<128, 4, true>(p, stream) : launch_t<128, 4, false>(p, stream);
   if (head_dim == 64 && group == 4)
     return trace ? launch_t<64, 4, true>(p, stream) : launch_t<64, 4, false>(p, stream);
-  if (head_dim == 128 && group == 8)
-    return trace ? launch_t<128, 8, true>(p, stream) : launch_t<128, 8, false>(p, stream);
   if (head_dim == 64 && group == 8)
     return trace ? launch_t<64, 8, true>(p, stream) : launch_t<64, 8, false>(p, stream);
   return hipErrorInvalidValue;

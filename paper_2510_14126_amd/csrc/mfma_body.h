@@ -1,0 +1,484 @@
+// Split-KV paged decode attention on MFMA tiles for GQA groups of 8 (gfx950).
+//
+// With eight query heads per KV head, QK^T and PV of a 16-token block are
+// dense enough for the matrix cores:
+//
+//  * S^T = K Q^T with v_mfma_f32_16x16x32_bf16: A = the K tile (16 tokens x 32
+//    dims per instruction, 4 instructions for D = 128), loaded straight from
+//    the pool in the same "token lane" order as the VALU kernel; B = Q^T with
+//    the eight query rows in columns 0..7 (columns 8..15 repeat them).  Lane
+//    (q, n) = (lane >> 4, lane & 15) receives scores of tokens 4q..4q+3 for
+//    query row n, which is exactly the A-operand layout of the PV product, so
+//    the probabilities never move between lanes.
+//  * O += P V with v_mfma_f32_16x16x16bf16_1k (one per 16 output dims): the
+//    B operand needs 4 consecutive tokens of one dim per lane, so the V tile is
+//    staged in LDS (row pitch 288 bytes) and read back with the transposing
+//    ds_read_b64_tr_b16, which hands lane (q, n) V[4q..4q+3][dim n].
+//
+// The online softmax keeps one running max per query row, replicated over the
+// four lane groups, and rescales the accumulator only when a block raises the
+// max by more than kLazyRescale (log2 units): probabilities stay <= 2^8, the
+// rescale branch is wave-uniform and rare.  P is rounded to bf16 for the
+// matrix core and the row sum adds the same rounded values, so the result is
+// an exact convex combination of the V rows up to fp32 accumulation.
+// Tail rows are removed by select: score -inf and V row zero.
+#pragma once
+
+#include "kernels.h"
+#include "pa_device.h"
+
+namespace pa {
+namespace mfma {
+
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) short4_t lds_short4_t;
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) u32x4_t lds_u32x4_t;
+
+constexpr int kD = 128;
+constexpr int kG = 8;
+constexpr int kWaves = 4;
+constexpr int kPitch = kD * 2 + 32;           // LDS bytes per staged V token row
+constexpr int kVTileBytes = 16 * kPitch;      // one staged V tile
+constexpr float kLazyRescale = 8.0f;
+#ifndef PA_MFMA_NBUF
+#define PA_MFMA_NBUF 3
+#endif
+constexpr int kNbuf = PA_MFMA_NBUF;  // tiles kept in flight per wavefront
+
+struct MfmaTile {
+  uint4 k[4];  // token n, K chunks 4s+q (16 bytes each)
+  uint4 v[4];  // token n, V chunks 4s+q
+};
+
+
+// Token n, chunks 4s+q of one K or V tile through a buffer descriptor built
+// from the wave-uniform tile address; `bytes` = 0 makes the loads no-ops that
+// return zeros but still count as issued.
+__device__ __forceinline__ void load_chunks(uint4 (&dst)[4], const uint16_t* tile, uint32_t lane_off,
+                                            int bytes) {
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(tile), 0, bytes, kBufferDescWord3);
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const auto x = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)lane_off + s * 64, 0, 0);
+    dst[s] = make_uint4(x[0], x[1], x[2], x[3]);
+  }
+}
+
+// Value of query column 4q+r (held by lane 4q+r) for the accumulator rows
+// of lane group q.
+__device__ __forceinline__ float column_value(float x, int q, int r) {
+  const int xi = __builtin_bit_cast(int, x);
+  const float c0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(xi, r));
+  const float c1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(xi, 4 + r));
+  const float c2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(xi, 8 + r));
+  const float c3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(xi, 12 + r));
+  return q == 0 ? c0 : (q == 1 ? c1 : (q == 2 ? c2 : c3));
+}
+
+// Online-softmax state of NT column tiles (16 query columns each).
+template <int NT>
+struct MfmaState {
+  float m[NT];        // running max of query column n (log2 units), same in all groups
+  float l[NT];        // this lane's share of the column sum (tokens 4q..4q+3 of each block)
+  floatx4_t o[NT][8]; // O[rows 4q+r][dims 16*blk + n] of each column tile
+};
+
+// One 16-token block against NT column tiles that share the K operand and
+// the staged V (their MFMA chains are independent and interleave).
+// `valid`: tokens of this tile that exist (V rows past it are zeroed);
+// `limit[t]`: tokens this lane's column of tile t may attend to (<= valid).
+template <bool TAIL, int NT>
+__device__ __forceinline__ void process_tile(MfmaState<NT>& S, const MfmaTile& T,
+                                             const uint4 (&qb)[NT][4], lds_u8_t* vbuf, int valid,
+                                             const int (&limit)[NT], int q, int n,
+                                             float scale_log2) {
+  // Stage V (token n, chunks 4s+q) into LDS; tail rows become zero.
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    u32x4_t v = {T.v[s].x, T.v[s].y, T.v[s].z, T.v[s].w};
+    if (TAIL && n >= valid) v = u32x4_t{0u, 0u, 0u, 0u};
+    *reinterpret_cast<lds_u32x4_t*>(vbuf + n * kPitch + (4 * s + q) * 16) = v;
+  }
+
+  floatx4_t st[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    st[t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, T.k[s]),
+                                                      __builtin_bit_cast(bf16x8_t, qb[t][s]), st[t],
+                                                      0, 0, 0);
+  }
+
+  float sc[NT][4], bm[NT];
+  bool raise = false;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    float b = -__builtin_inff();
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float x = st[t][r] * scale_log2;
+      if (TAIL && 4 * q + r >= limit[t]) x = -__builtin_inff();
+      sc[t][r] = x;
+      b = fmaxf(b, x);
+    }
+    bm[t] = group_max4(b);
+    raise |= bm[t] > S.m[t] + kLazyRescale;
+  }
+  if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const float mn = bm[t] > S.m[t] + kLazyRescale ? bm[t] : S.m[t];
+      // 1 for columns that keep their max (or have attended to nothing yet)
+      const float alpha = mn == -__builtin_inff() ? 1.f : fast_exp2(S.m[t] - mn);
+      S.l[t] *= alpha;
+      S.m[t] = mn;
+      // Accumulator rows are indexed by lane group: row 4q+r takes alpha of
+      // column 4q+r, held by lane 4q+r.
+      float ar[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) ar[r] = column_value(alpha, q, r);
+#pragma unroll
+      for (int blk = 0; blk < 8; ++blk)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) S.o[t][blk][r] *= ar[r];
+    }
+  }
+
+  // Probabilities, rounded to bf16 for the matrix core; the column sum uses
+  // the same rounded values.
+  short4_t pa[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const float mref = S.m[t] == -__builtin_inff() ? 0.f : S.m[t];  // fully masked: p = 0
+    float lsum = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const __bf16 pb = (__bf16)fast_exp2(sc[t][r] - mref);
+      lsum += (float)pb;
+      pa[t][r] = __builtin_bit_cast(short, pb);
+    }
+    S.l[t] += lsum;
+  }
+
+  // PV: B operand = V[4q..4q+3][16*blk + n] through the transposing LDS read.
+  // Source lane (q, n) points at token 4q + n/4, dims 16*blk + 4*(n%4).
+  lds_u8_t* src = vbuf + (4 * q + (n >> 2)) * kPitch + (n & 3) * 8;
+#pragma unroll
+  for (int blk = 0; blk < 8; ++blk) {
+    const short4_t vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        reinterpret_cast<lds_short4_t*>(src + blk * 32));
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      S.o[t][blk] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa[t], vb, S.o[t][blk], 0, 0, 0);
+  }
+}
+
+// LDS bytes either body needs (V staging, then the end-of-item merge).
+constexpr int kLdsBytes = kWaves * 2 * kVTileBytes;
+
+// One decode work item (partition, sequence, KV head) = workgroup `wg_index`.
+template <bool TRACE>
+__device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_index, lds_u8_t* smem) {
+  const int lane = threadIdx.x & 63;
+  const int wave = wave_uniform(threadIdx.x >> 6);
+  const int q = lane >> 4;
+  const int n = lane & 15;
+
+  int wg = wg_index;
+  const int g = wg % p.num_kv_heads;
+  wg /= p.num_kv_heads;
+  const int b = wg % p.batch;
+  const int part = wg / p.batch;
+
+  const int start = p.token_offset + part * p.part_tokens;
+  const int j0 = start >> 4;
+  const int h0 = g * kG;
+  const int32_t* bt = p.block_tables + (size_t)b * p.bt_stride + j0;
+  // The first 64 block ids and the query rows are loaded before the context
+  // length arrives (j0 < bt_stride for every launched partition).
+  const int raw_first = lane < min(64, p.bt_stride - j0) ? bt[lane] : 0;
+
+  // Q^T operand: column n holds query row n % 8; dims 32s + 8q .. +8.
+  uint4 qb[1][4];
+  {
+    const uint16_t* qrow = p.q + ((size_t)b * p.num_q_heads + h0 + (n & 7)) * kD;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) qb[0][s] = *reinterpret_cast<const uint4*>(qrow + (4 * s + q) * 8);
+  }
+
+  int ctx = p.context_lens[b];
+  ctx = ctx < 0 ? 0 : (ctx > p.max_ctx ? p.max_ctx : ctx);
+  const bool split = p.write_partials != 0;
+  if (split && start >= ctx) return;
+  const int end = min(ctx, start + p.part_tokens);
+  const int nblk = end > start ? (end - start + 15) >> 4 : 0;
+
+  lds_u8_t* lds = smem;
+  lds_u8_t* vbufs[2] = {lds + (wave * 2) * kVTileBytes, lds + (wave * 2 + 1) * kVTileBytes};
+
+  MfmaState<1> S;
+  S.m[0] = -__builtin_inff();
+  S.l[0] = 0.f;
+#pragma unroll
+  for (int blk = 0; blk < 8; ++blk) S.o[0][blk] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  constexpr size_t kTileElems = 16 * kD;
+  const size_t blk_stride = (size_t)p.num_kv_heads * kTileElems;
+  const uint16_t* kbase = p.k_pool + (size_t)g * kTileElems;
+  const uint16_t* vbase = p.v_pool + (size_t)g * kTileElems;
+  const size_t item = ((size_t)part * p.batch + b) * p.num_kv_heads + g;
+  const uint32_t lane_off = (uint32_t)(n * kD + q * 8) * 2u;  // token n, chunk q (+4s)
+  int flip = 0;
+
+  for (int c0 = 0; c0 < nblk; c0 += 64) {
+    const int cn = min(64, nblk - c0);
+    const int raw = c0 == 0 ? (lane < cn ? raw_first : 0) : (lane < cn ? bt[c0 + lane] : 0);
+    const int idc = min(max(raw, 0), p.num_blocks - 1);
+    auto load = [&](MfmaTile& T, int i) {
+      const bool ok = i < cn;
+      const size_t id = (size_t)__builtin_amdgcn_readlane(idc, ok ? i : 0);
+      const int bytes = ok ? (int)(kTileElems * 2) : 0;
+      load_chunks(T.k, kbase + id * blk_stride, lane_off, bytes);
+      load_chunks(T.v, vbase + id * blk_stride, lane_off, bytes);
+    };
+    auto run = [&](const MfmaTile& T, int i) {
+      const int valid = min(16, end - (start + (c0 + i) * 16));
+      lds_u8_t* vb = vbufs[flip];
+      flip ^= 1;
+      const int lim[1] = {valid};
+      if (valid == 16)
+        process_tile<false, 1>(S, T, qb, vb, 16, lim, q, n, p.scale_log2);
+      else
+        process_tile<true, 1>(S, T, qb, vb, valid, lim, q, n, p.scale_log2);
+      if constexpr (TRACE) {
+        if (lane == 0) {
+          int32_t* tr = p.trace + (item * p.trace_tiles + (c0 + i)) * 3;
+          tr[0] = j0 + c0 + i;
+          tr[1] = __builtin_amdgcn_readlane(raw, i);
+          tr[2] = valid;
+        }
+      }
+    };
+
+    int i = wave;
+    if (i >= cn) continue;
+    MfmaTile T[kNbuf];
+    int ld = i;
+#pragma unroll
+    for (int s = 0; s < kNbuf - 1; ++s) {
+      load(T[s], ld);
+      ld += kWaves;
+    }
+    bool done = false;
+    while (!done) {
+#pragma unroll
+      for (int s = 0; s < kNbuf; ++s) {
+        if (!done) {
+          load(T[(s + kNbuf - 1) % kNbuf], ld);
+          ld += kWaves;
+          run(T[s], i);
+          i += kWaves;
+          done = i >= cn;
+        }
+      }
+    }
+  }
+
+  // Merge the waves through LDS (the V staging area is free now).
+  const float lrow = group_sum4(S.l[0]);
+  __syncthreads();
+  lds_f32_t* sm = reinterpret_cast<lds_f32_t*>(smem);       // [W][8]
+  lds_f32_t* sl = sm + kWaves * kG;                          // [W][8]
+  lds_f32_t* sacc = sl + kWaves * kG;                        // [W][8][128]
+  if (q == 0 && n < kG) { sm[wave * kG + n] = S.m[0]; sl[wave * kG + n] = lrow; }
+  if (q < 2) {
+#pragma unroll
+    for (int blk = 0; blk < 8; ++blk)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        sacc[(wave * kG + 4 * q + r) * kD + 16 * blk + n] = S.o[0][blk][r];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+
+#pragma unroll
+  for (int r = 0; r < kG; ++r) {
+    float mx = sm[r];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) mx = fmaxf(mx, sm[w * kG + r]);
+    const float mref = (mx == -__builtin_inff()) ? 0.f : mx;
+    float lt = 0.f, o0 = 0.f, o1 = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float f = fast_exp2(sm[w * kG + r] - mref);
+      lt = fmaf(sl[w * kG + r], f, lt);
+      const float2 a = {sacc[(w * kG + r) * kD + 2 * lane], sacc[(w * kG + r) * kD + 2 * lane + 1]};
+      o0 = fmaf(a.x, f, o0);
+      o1 = fmaf(a.y, f, o1);
+    }
+    const float inv = lt > 0.f ? 1.0f / lt : 0.f;
+    if (!split) {
+      uint16_t* orow = p.out + ((size_t)b * p.num_q_heads + h0 + r) * kD;
+      *reinterpret_cast<uint32_t*>(orow + 2 * lane) = bf16_rne(o0 * inv) | (bf16_rne(o1 * inv) << 16);
+    } else {
+      const size_t row = ((size_t)b * p.num_q_heads + h0 + r) * p.part_stride + p.part_offset + part;
+      *reinterpret_cast<float2*>(p.part_o + row * kD + 2 * lane) = make_float2(o0 * inv, o1 * inv);
+      if (lane == 0)
+        p.part_lse[row] = lt > 0.f ? (mx + log2f(lt)) * kLn2 : -__builtin_inff();
+    }
+  }
+}
+
+// Attention over the prefix that every sequence of the batch shares: for KV
+// head g the B*G query rows form the columns of dense 16-row tiles (four
+// sequences of four heads, or two of eight, per tile).  One wavefront owns
+// kPrefixTiles column tiles (kPrefixTiles*16 query rows) that share each K
+// tile and staged V tile, and streams every block of one prefix partition for
+// them; the wavefronts of a workgroup read the same blocks, so each block
+// comes from HBM once and from L2 afterwards.  Every row writes its (o, lse)
+// partial for the partition, lse = -inf when it attended to nothing.
+constexpr int kPrefixTiles = 1;
+constexpr int kPrefixRowsPerWave = 16 * kPrefixTiles;
+#ifndef PA_PREFIX_NBUF
+#define PA_PREFIX_NBUF 3
+#endif
+constexpr int kPrefixNbuf = PA_PREFIX_NBUF;  // tiles in flight per prefix wavefront
+
+template <int G>
+__device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_index, lds_u8_t* smem) {
+  constexpr int NT = kPrefixTiles;
+  const int lane = threadIdx.x & 63;
+  const int wave = wave_uniform(threadIdx.x >> 6);
+  const int q = lane >> 4;
+  const int n = lane & 15;
+
+  const int total_rows = p.batch * G;
+  const int row_groups = (total_rows + kPrefixRowsPerWave * kWaves - 1) / (kPrefixRowsPerWave * kWaves);
+  int wg = wg_index;
+  const int g = wg % p.num_kv_heads;
+  wg /= p.num_kv_heads;
+  const int rg = wg % row_groups;
+  const int part = wg / row_groups;
+  const int row0 = (rg * kWaves + wave) * kPrefixRowsPerWave;
+  if (row0 >= total_rows) return;               // no barrier below: waves are independent
+
+  const int start = part * p.part_tokens;
+  const int end = min(p.prefix_len, start + p.part_tokens);
+  const int nblk = (end - start + 15) >> 4;     // >= 1 for every launched partition
+  const int raw = lane < nblk ? p.block_tables[(start >> 4) + lane] : 0;
+  const int idc = min(max(raw, 0), p.num_blocks - 1);
+
+  // Column n of tile t is query row R = row0 + 16t + n: sequence R / G,
+  // head g*G + R % G.
+  uint4 qb[NT][4];
+  int ctx[NT];
+  bool col_ok[NT];
+  int min_ctx = 0x7fffffff;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int R = row0 + 16 * t + n;
+    col_ok[t] = R < total_rows;
+    const int bR = col_ok[t] ? R / G : 0;
+    const int hR = g * G + R % G;
+    const uint16_t* qrow = p.q + ((size_t)bR * p.num_q_heads + hR) * kD;
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      qb[t][s] = col_ok[t] ? *reinterpret_cast<const uint4*>(qrow + (4 * s + q) * 8)
+                           : make_uint4(0, 0, 0, 0);
+    int c = col_ok[t] ? p.context_lens[bR] : 0;
+    c = c < 0 ? 0 : (c > p.max_ctx ? p.max_ctx : c);
+    ctx[t] = c;
+    // shortest context among the tile's columns (decides when to mask)
+    min_ctx = min(min_ctx, __builtin_amdgcn_readfirstlane(-(int)group_max4(row_max16(-(float)c))));
+  }
+
+  lds_u8_t* lds = smem;
+  lds_u8_t* vbufs[2] = {lds + (wave * 2) * kVTileBytes, lds + (wave * 2 + 1) * kVTileBytes};
+
+  MfmaState<NT> S;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    S.m[t] = -__builtin_inff();
+    S.l[t] = 0.f;
+#pragma unroll
+    for (int blk = 0; blk < 8; ++blk) S.o[t][blk] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  }
+
+  constexpr size_t kTileElems = 16 * kD;
+  const size_t blk_stride = (size_t)p.num_kv_heads * kTileElems;
+  const uint16_t* kbase = p.k_pool + (size_t)g * kTileElems;
+  const uint16_t* vbase = p.v_pool + (size_t)g * kTileElems;
+  const uint32_t lane_off = (uint32_t)(n * kD + q * 8) * 2u;
+  int flip = 0;
+
+  auto load = [&](MfmaTile& T, int i) {
+    const bool ok = i < nblk;
+    const size_t id = (size_t)__builtin_amdgcn_readlane(idc, ok ? i : 0);
+    const int bytes = ok ? (int)(kTileElems * 2) : 0;
+    load_chunks(T.k, kbase + id * blk_stride, lane_off, bytes);
+    load_chunks(T.v, vbase + id * blk_stride, lane_off, bytes);
+  };
+  auto run = [&](const MfmaTile& T, int i) {
+    const int t0 = start + i * 16;
+    const int valid = min(16, end - t0);
+    lds_u8_t* vb = vbufs[flip];
+    flip ^= 1;
+    int lim[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) lim[t] = min(valid, max(ctx[t] - t0, 0));
+    if (valid == 16 && min_ctx - t0 >= 16)
+      process_tile<false, NT>(S, T, qb, vb, 16, lim, q, n, p.scale_log2);
+    else
+      process_tile<true, NT>(S, T, qb, vb, valid, lim, q, n, p.scale_log2);
+  };
+
+  MfmaTile T[kPrefixNbuf];
+  int ld = 0, i = 0;
+#pragma unroll
+  for (int s = 0; s < kPrefixNbuf - 1; ++s) load(T[s], ld++);
+  bool done = false;
+  while (!done) {
+#pragma unroll
+    for (int s = 0; s < kPrefixNbuf; ++s) {
+      if (!done) {
+        load(T[(s + kPrefixNbuf - 1) % kPrefixNbuf], ld++);
+        run(T[s], i);
+        ++i;
+        done = i >= nblk;
+      }
+    }
+  }
+
+  // Normalise per row and write this partition's partials.
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const float lrow = group_sum4(S.l[t]);
+    const float inv = lrow > 0.f ? 1.0f / lrow : 0.f;
+    const int R = row0 + 16 * t + n;
+    if (q == 0 && col_ok[t]) {
+      const size_t row = ((size_t)(R / G) * p.num_q_heads + g * G + R % G) * p.part_stride + part;
+      p.part_lse[row] = lrow > 0.f ? (S.m[t] + log2f(lrow)) * kLn2 : -__builtin_inff();
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int Rr = row0 + 16 * t + 4 * q + r;
+      const float f = column_value(inv, q, r);
+      if (Rr < total_rows) {
+        const size_t row = ((size_t)(Rr / G) * p.num_q_heads + g * G + Rr % G) * p.part_stride + part;
+        float* po = p.part_o + row * kD + n;
+#pragma unroll
+        for (int blk = 0; blk < 8; ++blk) po[16 * blk] = S.o[t][blk][r] * f;
+      }
+    }
+  }
+}
+
+}  // namespace mfma
+}  // namespace pa

@@ -41,6 +41,10 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // format, no swizzle); the first three hold the base and the byte size.
 constexpr int kBufferDescWord3 = 0x00020000;
 
+// LDS (address space 3) pointer types.
+typedef __attribute__((address_space(3))) uint8_t lds_u8_t;
+typedef __attribute__((address_space(3))) float lds_f32_t;
+
 // ---- cross-lane movement ---------------------------------------------------
 
 // DPP controls (gfx9 encoding).
