@@ -37,15 +37,34 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 PROFILE_DIR = os.path.join(ROOT, "profiles")
+_CSRC = "paper_2510_14126_amd/csrc/"
 KERNEL_SOURCES = {
-    "decode_valu": ["paper_2510_14126_amd/csrc/decode_valu.hip", "paper_2510_14126_amd/csrc/pa_device.h"],
-    "decode_mfma": ["paper_2510_14126_amd/csrc/decode_mfma.hip", "paper_2510_14126_amd/csrc/pa_device.h"],
+    "decode_valu": [_CSRC + f for f in ("decode_valu.hip", "valu_body.h", "pa_device.h", "kernels.h")],
+    "decode_mfma": [_CSRC + f for f in ("decode_mfma.hip", "mfma_body.h", "pa_device.h", "kernels.h")],
+    "cascade": [_CSRC + f for f in ("cascade.hip", "valu_body.h", "mfma_body.h", "pa_device.h",
+                                    "kernels.h")],
 }
+# Split-KV partition sizes used when --partition-size is not given.  The
+# long-context pool states 512-token partitions; the other workloads state
+# none and use the size that measured fastest on them.
+DEFAULT_PARTITION = {1: 512, 2: 512, 3: 1024, 4: 1024, 5: 512}
 
 
-def decode_kernel_of(w) -> str:
+def default_prefix_partition(prefix_len: int) -> int:
+    """Prefix partition: a quarter of the shared prefix, within [256, 1024] tokens."""
+    return max(256, min(1024, (prefix_len // 4) // 16 * 16))
+
+
+def decode_kernel_of(w, prefix_len: int = 0) -> str:
     """Which decode kernel the library launches for this geometry."""
+    if prefix_len:
+        return "cascade"
     return "decode_mfma" if (w.group == 8 and w.head_dim == 128) else "decode_valu"
+
+
+def kernel_display_name(w, kernel: str) -> str:
+    return {"cascade": f"cascade_kernel<{w.group}>", "decode_mfma": "decode_mfma_g8_kernel",
+            "decode_valu": f"decode_valu_kernel<{w.head_dim},{w.group}>"}[kernel]
 
 
 def log(msg):
@@ -207,6 +226,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--hot", action="store_true", help="also time steps on a single replica")
+    ap.add_argument("--cascade", choices=["auto", "on", "off"], default="auto",
+                    help="shared-prefix cascade (auto: on when the batch shares a prefix)")
+    ap.add_argument("--prefix-partition-size", type=int, default=None,
+                    help="tokens per prefix partition (default: a quarter of the prefix, 256..1024)")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay each step from a captured HIP graph (one per replica)")
     ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--ingest-stats", metavar="KERNEL_STATS_CSV")
     ap.add_argument("--command-note", default="")
@@ -220,8 +245,9 @@ def main():
         name = CONFIG_NAMES[args.config]
         if args.ingest_counters:
             from workloads import build_config
-            kern = decode_kernel_of(build_config(args.config, values=False))
-            ingest_counters(*args.ingest_counters, name, kern, args.command_note)
+            wc = build_config(args.config, values=False)
+            plen = 0 if args.cascade == "off" else 16 * int(wc.meta.get("prefix_blocks", 0))
+            ingest_counters(*args.ingest_counters, name, decode_kernel_of(wc, plen), args.command_note)
         if args.ingest_stats:
             ingest_stats(args.ingest_stats, name, args.command_note)
         return
@@ -235,8 +261,7 @@ def main():
     from workloads import build_config
     t0 = time.perf_counter()
     w = build_config(args.config)
-    if args.partition_size is not None:
-        w.partition_size = args.partition_size
+    w.partition_size = args.partition_size or DEFAULT_PARTITION.get(args.config, w.partition_size)
     alg_bytes, logical_bytes = byte_accounting(w)
     log(f"workload {w.name}: B={w.batch} Hq={w.num_q_heads} Hkv={w.num_kv_heads} D={w.head_dim} "
         f"NB={w.num_blocks} max_ctx={w.max_context_len} alg={alg_bytes/1e6:.1f} MB "
@@ -255,7 +280,11 @@ def main():
     dev = torch.device("cuda:0")
     pool_bytes = 2 * w.k_pool.nbytes
     R = args.replicas or max(1, min(16, -(-(1 << 30) // pool_bytes)))
-    base = PagedBatch(w, dev)
+    prefix_len = 16 * int(w.meta.get("prefix_blocks", 0))
+    if args.cascade == "off" or (args.cascade == "auto" and prefix_len == 0):
+        prefix_len = 0
+    pps = args.prefix_partition_size or default_prefix_partition(prefix_len)
+    base = PagedBatch(w, dev, prefix_len=prefix_len, prefix_partition_size=pps)
     reps = [(base.pool, base.q)]
     keep = []
     for _ in range(1, R):
@@ -265,17 +294,28 @@ def main():
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
-    split = base.num_parts > 1
+    split = base.needs_reduce
+
+    def decode_on(i, s):
+        pool, q = reps[i % R]
+        if prefix_len:
+            binding.paged_attn_decode_cascade(pool, q, base.bt, base.bt_stride, base.ctx, base.batch,
+                                              base.hq, w.scale, base.max_ctx, base.partition_size,
+                                              prefix_len, base.prefix_partition_size, base.part_o,
+                                              base.part_lse, s)
+        else:
+            binding.paged_attn_decode(pool, q, base.bt, base.bt_stride, base.ctx, base.batch,
+                                      base.hq, w.scale, base.max_ctx, base.partition_size,
+                                      base.out, base.part_o, base.part_lse, s)
+
+    def reduce_on(s):
+        base.reduce(s)
 
     def decode(i):
-        pool, q = reps[i % R]
-        binding.paged_attn_decode(pool, q, base.bt, base.bt_stride, base.ctx, base.batch, base.hq,
-                                  w.scale, base.max_ctx, base.partition_size, base.out,
-                                  base.part_o, base.part_lse, sh)
+        decode_on(i, sh)
 
     def reduce():
-        binding.paged_attn_reduce(base.part_o, base.part_lse, base.ctx, base.batch, base.hq,
-                                  base.d, base.partition_size, base.num_parts, base.out, sh)
+        reduce_on(sh)
 
     if args.profile_loop:
         src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
@@ -297,33 +337,63 @@ def main():
     torch.cuda.synchronize()
 
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    step_fn = [None] * R
+    if args.graph:
+        # one captured step per replica; replays carry no host launch cost
+        for r in range(R):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                cs = torch.cuda.current_stream().cuda_stream
+                decode_on(r, cs)
+                if split:
+                    reduce_on(cs)
+            step_fn[r] = g
+        for r in range(R):
+            step_fn[r].replay()
+        torch.cuda.synchronize()
+
+    def step(i):
+        if args.graph:
+            step_fn[i % R].replay()
+        else:
+            decode(i)
+            if split:
+                reduce()
+
+    # timed region: K whole steps, no instrumentation between launches
+    e_start = torch.cuda.Event(enable_timing=True)
+    e_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
+    e_start.record(stream)
     for i in range(K):
-        e = ev[i]
-        e[0].record(stream)
-        decode(i)
-        e[1].record(stream)
-        if split:
-            reduce()
-        e[2].record(stream)
+        step(i)
+    e_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
-    dec_ms = np.array([ev[i][0].elapsed_time(ev[i][1]) for i in range(K)])
-    red_ms = np.array([ev[i][1].elapsed_time(ev[i][2]) for i in range(K)])
-    span_ms = ev[0][0].elapsed_time(ev[K - 1][2])
-    ms_step = span_ms / K
+    ms_step = e_start.elapsed_time(e_end) / K
+
+    # per-kernel durations: K decode launches back to back between two events
+    # on the launch stream, then K reduce launches the same way
+    e_dec = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    torch.cuda.synchronize()
+    e_dec[0].record(stream)
+    for i in range(K):
+        decode(i)
+    e_dec[1].record(stream)
+    for i in range(K if split else 0):
+        reduce()
+    e_dec[2].record(stream)
+    torch.cuda.synchronize()
+    dec_avg = e_dec[0].elapsed_time(e_dec[1]) / K
+    red_avg = e_dec[1].elapsed_time(e_dec[2]) / K if split else 0.0
 
     # hot: one replica, same loop (optional)
     hot = []
     for i in range(K if args.hot else 0):
         e0 = torch.cuda.Event(enable_timing=True); e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        pool, q = reps[0]
-        binding.paged_attn_decode(pool, q, base.bt, base.bt_stride, base.ctx, base.batch, base.hq,
-                                  w.scale, base.max_ctx, base.partition_size, base.out,
-                                  base.part_o, base.part_lse, sh)
+        decode(0)
         if split:
             reduce()
         e1.record(stream)
@@ -358,10 +428,9 @@ def main():
     rep = compare(base.out_bits()[seqs], ref)
     log(f"parity spot check on sequences {seqs}: {rep}")
 
-    dec_avg = float(dec_ms.mean())
     achieved = alg_bytes / (dec_avg * 1e-3) / 1e9
     value = alg_bytes / (ms_step * 1e-3) / 1e9
-    kern = decode_kernel_of(w)
+    kern = decode_kernel_of(w, prefix_len)
     traffic = traffic_from_profiles(w.name, kern)
     line = {
         "metric": "paged decode-attention KV GB/s (algorithmic bytes) and % of HBM peak; "
@@ -381,6 +450,9 @@ def main():
                    "num_q_heads": w.num_q_heads, "num_kv_heads": w.num_kv_heads,
                    "head_dim": w.head_dim, "block_size": 16, "partition_size": base.partition_size,
                    "num_partitions": base.num_parts, "replicas_rotated": R,
+                   "shared_prefix_cascade": {"prefix_len": prefix_len,
+                                             "prefix_partition_size": base.prefix_partition_size}
+                   if prefix_len else None,
                    "max_context_len": w.max_context_len, "parallelism": "single GPU"},
         "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "decode_steps_per_s": round(1000.0 / ms_step, 2),
@@ -388,7 +460,8 @@ def main():
         "algorithmic_bytes_per_step": int(alg_bytes),
         "logical_kv_gbps_effective": round(logical_bytes / (ms_step * 1e-3) / 1e9, 2),
         "hot_ms_per_step": round(hot_ms, 5) if hot_ms is not None else None,
-        "kernel_ms": {"decode_avg": round(dec_avg, 5), "reduce_avg": round(float(red_ms.mean()), 5)},
+        "launch": "hip graph replay per step" if args.graph else "direct launches",
+        "kernel_ms": {"decode_avg": round(dec_avg, 5), "reduce_avg": round(red_avg, 5)},
         "copy_probe_gbps": round(copy_gbps, 1),
         "pct_of_copy_probe": round(100 * value / copy_gbps, 2),
         "wall_s_timed_region": round(wall, 4),
@@ -397,8 +470,8 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic,
-                     "kernel": ("decode_mfma_g8_kernel" if kern == "decode_mfma"
-                                else f"decode_valu_kernel<{w.head_dim},{w.group}>"),
+                     "kernel": kernel_display_name(w, kern),
+                     "launch": "decode call (all kernels it launches)",
                      "bytes_per_launch": int(alg_bytes)},
         "cpu_baseline": cpu,
     }

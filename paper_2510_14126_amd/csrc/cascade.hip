@@ -37,7 +37,7 @@ cascade_kernel(const PrefixParams pp, const DecodeParams dp, int prefix_wgs) {
 hipError_t launch_cascade(const PrefixParams& pp, const DecodeParams& dp, int group,
                           hipStream_t stream) {
   const int64_t rows = (int64_t)pp.batch * group;
-  const int64_t row_groups = (rows + mfma::kPrefixRowsPerWave * mfma::kWaves - 1) / (mfma::kPrefixRowsPerWave * mfma::kWaves);
+  const int64_t row_groups = (rows + mfma::kPrefixRowsPerWg - 1) / mfma::kPrefixRowsPerWg;
   const int64_t prefix_wgs = (int64_t)pp.prefix_parts * row_groups * pp.num_kv_heads;
   const int64_t decode_wgs = (int64_t)dp.num_parts * dp.batch * dp.num_kv_heads;
   const int64_t grid = prefix_wgs + decode_wgs;

@@ -25,7 +25,7 @@ prefix_mfma_kernel(const PrefixParams p) {
 
 hipError_t launch_prefix_mfma(const PrefixParams& p, int group, hipStream_t stream) {
   const int64_t rows = (int64_t)p.batch * group;
-  const int64_t row_groups = (rows + mfma::kPrefixRowsPerWave * kWaves - 1) / (mfma::kPrefixRowsPerWave * kWaves);
+  const int64_t row_groups = (rows + mfma::kPrefixRowsPerWg - 1) / mfma::kPrefixRowsPerWg;
   const int64_t grid = (int64_t)p.prefix_parts * row_groups * p.num_kv_heads;
   if (grid == 0) return hipSuccess;
   if (group == 4)

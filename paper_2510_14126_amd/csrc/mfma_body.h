@@ -3,16 +3,23 @@
 // With eight query heads per KV head, QK^T and PV of a 16-token block are
 // dense enough for the matrix cores:
 //
+//  * Both tiles of a block are read from the pool in row order: each 16-lane
+//    group takes one whole 256-byte token row, so a load instruction reads
+//    1 KiB of contiguous memory and the vector L1 sees one access per 64
+//    bytes.  (Reading the MFMA operand layout straight from the pool would
+//    put 16 different rows in every 16-lane group, about one L1 access per
+//    lane, and the L1 becomes the limit when the tiles come from L2.)  The
+//    block is staged in LDS and each lane reads its operands from there.
 //  * S^T = K Q^T with v_mfma_f32_16x16x32_bf16: A = the K tile (16 tokens x 32
-//    dims per instruction, 4 instructions for D = 128), loaded straight from
-//    the pool in the same "token lane" order as the VALU kernel; B = Q^T with
-//    the eight query rows in columns 0..7 (columns 8..15 repeat them).  Lane
-//    (q, n) = (lane >> 4, lane & 15) receives scores of tokens 4q..4q+3 for
-//    query row n, which is exactly the A-operand layout of the PV product, so
-//    the probabilities never move between lanes.
+//    dims per instruction, 4 instructions for D = 128), read from LDS (row
+//    pitch 272 bytes: the 16 rows of a column fall in distinct banks); B = Q^T
+//    with the query rows in its 16 columns.  Lane (q, n) = (lane >> 4,
+//    lane & 15) receives scores of tokens 4q..4q+3 for query column n, which
+//    is exactly the A-operand layout of the PV product, so the probabilities
+//    never move between lanes.
 //  * O += P V with v_mfma_f32_16x16x16bf16_1k (one per 16 output dims): the
-//    B operand needs 4 consecutive tokens of one dim per lane, so the V tile is
-//    staged in LDS (row pitch 288 bytes) and read back with the transposing
+//    B operand needs 4 consecutive tokens of one dim per lane; the staged V
+//    tile (row pitch 288 bytes) is read back with the transposing
 //    ds_read_b64_tr_b16, which hands lane (q, n) V[4q..4q+3][dim n].
 //
 // The online softmax keeps one running max per query row, replicated over the
@@ -43,6 +50,9 @@ constexpr int kG = 8;
 constexpr int kWaves = 4;
 constexpr int kPitch = kD * 2 + 32;           // LDS bytes per staged V token row
 constexpr int kVTileBytes = 16 * kPitch;      // one staged V tile
+constexpr int kKPitch = kD * 2 + 16;          // LDS bytes per staged K token row
+constexpr int kKTileBytes = 16 * kKPitch;     // one staged K tile
+constexpr int kStageBytes = kKTileBytes + kVTileBytes;  // one staged block: K, then V
 constexpr float kLazyRescale = 8.0f;
 #ifndef PA_MFMA_NBUF
 #define PA_MFMA_NBUF 3
@@ -50,22 +60,23 @@ constexpr float kLazyRescale = 8.0f;
 constexpr int kNbuf = PA_MFMA_NBUF;  // tiles kept in flight per wavefront
 
 struct MfmaTile {
-  uint4 k[4];  // token n, K chunks 4s+q (16 bytes each)
-  uint4 v[4];  // token n, V chunks 4s+q
+  uint4 k[4];  // [u]: row 4u+q, 16-byte chunk n of the K tile
+  uint4 v[4];  // [u]: row 4u+q, chunk n of the V tile
 };
 
 
-// Token n, chunks 4s+q of one K or V tile through a buffer descriptor built
-// from the wave-uniform tile address; `bytes` = 0 makes the loads no-ops that
-// return zeros but still count as issued.
+// Rows 4u+q, chunk n of one K or V tile (lane_off = the byte offset of row q,
+// chunk n) through a buffer descriptor built from the wave-uniform tile
+// address; `bytes` = 0 makes the loads no-ops that return zeros but still
+// count as issued.
 __device__ __forceinline__ void load_chunks(uint4 (&dst)[4], const uint16_t* tile, uint32_t lane_off,
                                             int bytes) {
   const __amdgpu_buffer_rsrc_t rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(tile), 0, bytes, kBufferDescWord3);
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    const auto x = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)lane_off + s * 64, 0, 0);
-    dst[s] = make_uint4(x[0], x[1], x[2], x[3]);
+  for (int u = 0; u < 4; ++u) {
+    const auto x = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)lane_off + u * 4 * kD * 2, 0, 0);
+    dst[u] = make_uint4(x[0], x[1], x[2], x[3]);
   }
 }
 
@@ -90,20 +101,30 @@ struct MfmaState {
 
 // One 16-token block against NT column tiles that share the K operand and
 // the staged V (their MFMA chains are independent and interleave).
-// `valid`: tokens of this tile that exist (V rows past it are zeroed);
-// `limit[t]`: tokens this lane's column of tile t may attend to (<= valid).
+// `stage`: kStageBytes of this wavefront's LDS; `valid`: tokens of this tile
+// that exist (V rows past it are zeroed); `limit[t]`: tokens this lane's
+// column of tile t may attend to (<= valid).
 template <bool TAIL, int NT>
 __device__ __forceinline__ void process_tile(MfmaState<NT>& S, const MfmaTile& T,
-                                             const uint4 (&qb)[NT][4], lds_u8_t* vbuf, int valid,
+                                             const uint4 (&qb)[NT][4], lds_u8_t* stage, int valid,
                                              const int (&limit)[NT], int q, int n,
                                              float scale_log2) {
-  // Stage V (token n, chunks 4s+q) into LDS; tail rows become zero.
+  lds_u8_t* kbuf = stage;
+  lds_u8_t* vbuf = stage + kKTileBytes;
+  // Stage the block (rows 4u+q, chunk n); V tail rows become zero.
 #pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    u32x4_t v = {T.v[s].x, T.v[s].y, T.v[s].z, T.v[s].w};
-    if (TAIL && n >= valid) v = u32x4_t{0u, 0u, 0u, 0u};
-    *reinterpret_cast<lds_u32x4_t*>(vbuf + n * kPitch + (4 * s + q) * 16) = v;
+  for (int u = 0; u < 4; ++u) {
+    const u32x4_t k = {T.k[u].x, T.k[u].y, T.k[u].z, T.k[u].w};
+    *reinterpret_cast<lds_u32x4_t*>(kbuf + (4 * u + q) * kKPitch + n * 16) = k;
+    u32x4_t v = {T.v[u].x, T.v[u].y, T.v[u].z, T.v[u].w};
+    if (TAIL && 4 * u + q >= valid) v = u32x4_t{0u, 0u, 0u, 0u};
+    *reinterpret_cast<lds_u32x4_t*>(vbuf + (4 * u + q) * kPitch + n * 16) = v;
   }
+  // A operand of k-step s: token n, dims 32s + 8q .. +8 (chunk 4s+q).
+  u32x4_t ka[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    ka[s] = *reinterpret_cast<const lds_u32x4_t*>(kbuf + n * kKPitch + (4 * s + q) * 16);
 
   floatx4_t st[NT];
 #pragma unroll
@@ -111,7 +132,7 @@ __device__ __forceinline__ void process_tile(MfmaState<NT>& S, const MfmaTile& T
     st[t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < 4; ++s)
-      st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, T.k[s]),
+      st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[s]),
                                                       __builtin_bit_cast(bf16x8_t, qb[t][s]), st[t],
                                                       0, 0, 0);
   }
@@ -180,8 +201,9 @@ __device__ __forceinline__ void process_tile(MfmaState<NT>& S, const MfmaTile& T
   }
 }
 
-// LDS bytes either body needs (V staging, then the end-of-item merge).
-constexpr int kLdsBytes = kWaves * 2 * kVTileBytes;
+// LDS bytes either body needs (two staged blocks per wavefront, then the
+// end-of-item merge).
+constexpr int kLdsBytes = kWaves * 2 * kStageBytes;
 
 // One decode work item (partition, sequence, KV head) = workgroup `wg_index`.
 template <bool TRACE>
@@ -221,7 +243,7 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
   const int nblk = end > start ? (end - start + 15) >> 4 : 0;
 
   lds_u8_t* lds = smem;
-  lds_u8_t* vbufs[2] = {lds + (wave * 2) * kVTileBytes, lds + (wave * 2 + 1) * kVTileBytes};
+  lds_u8_t* stages[2] = {lds + (wave * 2) * kStageBytes, lds + (wave * 2 + 1) * kStageBytes};
 
   MfmaState<1> S;
   S.m[0] = -__builtin_inff();
@@ -234,7 +256,7 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
   const uint16_t* kbase = p.k_pool + (size_t)g * kTileElems;
   const uint16_t* vbase = p.v_pool + (size_t)g * kTileElems;
   const size_t item = ((size_t)part * p.batch + b) * p.num_kv_heads + g;
-  const uint32_t lane_off = (uint32_t)(n * kD + q * 8) * 2u;  // token n, chunk q (+4s)
+  const uint32_t lane_off = (uint32_t)(q * kD + n * 8) * 2u;  // row q, chunk n (+ 4 rows per u)
   int flip = 0;
 
   for (int c0 = 0; c0 < nblk; c0 += 64) {
@@ -250,7 +272,7 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
     };
     auto run = [&](const MfmaTile& T, int i) {
       const int valid = min(16, end - (start + (c0 + i) * 16));
-      lds_u8_t* vb = vbufs[flip];
+      lds_u8_t* vb = stages[flip];
       flip ^= 1;
       const int lim[1] = {valid};
       if (valid == 16)
@@ -291,7 +313,7 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
     }
   }
 
-  // Merge the waves through LDS (the V staging area is free now).
+  // Merge the waves through LDS (the staging area is free now).
   const float lrow = group_sum4(S.l[0]);
   __syncthreads();
   lds_f32_t* sm = reinterpret_cast<lds_f32_t*>(smem);       // [W][8]
@@ -338,36 +360,30 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
 
 // Attention over the prefix that every sequence of the batch shares: for KV
 // head g the B*G query rows form the columns of dense 16-row tiles (four
-// sequences of four heads, or two of eight, per tile).  One wavefront owns
-// kPrefixTiles column tiles (kPrefixTiles*16 query rows) that share each K
-// tile and staged V tile, and streams every block of one prefix partition for
-// them; the wavefronts of a workgroup read the same blocks, so each block
-// comes from HBM once and from L2 afterwards.  Every row writes its (o, lse)
-// partial for the partition, lse = -inf when it attended to nothing.
-constexpr int kPrefixTiles = 1;
-constexpr int kPrefixRowsPerWave = 16 * kPrefixTiles;
-#ifndef PA_PREFIX_NBUF
-#define PA_PREFIX_NBUF 3
-#endif
-constexpr int kPrefixNbuf = PA_PREFIX_NBUF;  // tiles in flight per prefix wavefront
+// sequences of four heads, or two of eight, per tile).  One workgroup owns one
+// column tile and one prefix partition; its wavefronts take the partition's
+// blocks round-robin, as the decode bodies do, and merge through LDS.  All
+// column tiles of a KV head read the same blocks, so each block comes from
+// HBM once and from L2 afterwards.  Every row writes its (o, lse) partial for
+// the partition, lse = -inf when it attended to nothing.
+constexpr int kPrefixRowsPerWg = 16;
+static_assert((2 * kWaves * 16 + kWaves * 16 * kD) * 4 <= kLdsBytes, "prefix merge must fit in LDS");
 
 template <int G>
 __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_index, lds_u8_t* smem) {
-  constexpr int NT = kPrefixTiles;
   const int lane = threadIdx.x & 63;
   const int wave = wave_uniform(threadIdx.x >> 6);
   const int q = lane >> 4;
   const int n = lane & 15;
 
   const int total_rows = p.batch * G;
-  const int row_groups = (total_rows + kPrefixRowsPerWave * kWaves - 1) / (kPrefixRowsPerWave * kWaves);
+  const int tiles = (total_rows + kPrefixRowsPerWg - 1) / kPrefixRowsPerWg;
   int wg = wg_index;
   const int g = wg % p.num_kv_heads;
   wg /= p.num_kv_heads;
-  const int rg = wg % row_groups;
-  const int part = wg / row_groups;
-  const int row0 = (rg * kWaves + wave) * kPrefixRowsPerWave;
-  if (row0 >= total_rows) return;               // no barrier below: waves are independent
+  const int tile = wg % tiles;
+  const int part = wg / tiles;
+  const int row0 = tile * kPrefixRowsPerWg;
 
   const int start = part * p.part_tokens;
   const int end = min(p.prefix_len, start + p.part_tokens);
@@ -375,108 +391,123 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
   const int raw = lane < nblk ? p.block_tables[(start >> 4) + lane] : 0;
   const int idc = min(max(raw, 0), p.num_blocks - 1);
 
-  // Column n of tile t is query row R = row0 + 16t + n: sequence R / G,
-  // head g*G + R % G.
-  uint4 qb[NT][4];
-  int ctx[NT];
-  bool col_ok[NT];
-  int min_ctx = 0x7fffffff;
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    const int R = row0 + 16 * t + n;
-    col_ok[t] = R < total_rows;
-    const int bR = col_ok[t] ? R / G : 0;
-    const int hR = g * G + R % G;
-    const uint16_t* qrow = p.q + ((size_t)bR * p.num_q_heads + hR) * kD;
+  // Column n is query row R = row0 + n: sequence R / G, head g*G + R % G.
+  uint4 qb[1][4];
+  int ctx;
+  int min_ctx;
+  {
+    const int R = row0 + n;
+    const bool ok = R < total_rows;
+    const int bR = ok ? R / G : 0;
+    const uint16_t* qrow = p.q + ((size_t)bR * p.num_q_heads + g * G + R % G) * kD;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
-      qb[t][s] = col_ok[t] ? *reinterpret_cast<const uint4*>(qrow + (4 * s + q) * 8)
-                           : make_uint4(0, 0, 0, 0);
-    int c = col_ok[t] ? p.context_lens[bR] : 0;
+      qb[0][s] = ok ? *reinterpret_cast<const uint4*>(qrow + (4 * s + q) * 8) : make_uint4(0, 0, 0, 0);
+    int c = ok ? p.context_lens[bR] : 0;
     c = c < 0 ? 0 : (c > p.max_ctx ? p.max_ctx : c);
-    ctx[t] = c;
+    ctx = c;
     // shortest context among the tile's columns (decides when to mask)
-    min_ctx = min(min_ctx, __builtin_amdgcn_readfirstlane(-(int)group_max4(row_max16(-(float)c))));
+    min_ctx = __builtin_amdgcn_readfirstlane(-(int)group_max4(row_max16(-(float)c)));
   }
 
-  lds_u8_t* lds = smem;
-  lds_u8_t* vbufs[2] = {lds + (wave * 2) * kVTileBytes, lds + (wave * 2 + 1) * kVTileBytes};
+  lds_u8_t* stages[2] = {smem + (wave * 2) * kStageBytes, smem + (wave * 2 + 1) * kStageBytes};
 
-  MfmaState<NT> S;
+  MfmaState<1> S;
+  S.m[0] = -__builtin_inff();
+  S.l[0] = 0.f;
 #pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    S.m[t] = -__builtin_inff();
-    S.l[t] = 0.f;
-#pragma unroll
-    for (int blk = 0; blk < 8; ++blk) S.o[t][blk] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-  }
+  for (int blk = 0; blk < 8; ++blk) S.o[0][blk] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
   constexpr size_t kTileElems = 16 * kD;
   const size_t blk_stride = (size_t)p.num_kv_heads * kTileElems;
   const uint16_t* kbase = p.k_pool + (size_t)g * kTileElems;
   const uint16_t* vbase = p.v_pool + (size_t)g * kTileElems;
-  const uint32_t lane_off = (uint32_t)(n * kD + q * 8) * 2u;
+  const uint32_t lane_off = (uint32_t)(q * kD + n * 8) * 2u;  // row q, chunk n (+ 4 rows per u)
   int flip = 0;
 
+  // The column tiles of a KV head walk the partition from evenly spread
+  // starting blocks, so at any moment they read different blocks instead of
+  // all queueing on the L2 lines of the same one.
+  const int rot = (int)(((int64_t)tile * nblk) / tiles) % nblk;
+  auto block_of = [&](int i) { const int j = i + rot; return j >= nblk ? j - nblk : j; };
   auto load = [&](MfmaTile& T, int i) {
     const bool ok = i < nblk;
-    const size_t id = (size_t)__builtin_amdgcn_readlane(idc, ok ? i : 0);
+    const size_t id = (size_t)__builtin_amdgcn_readlane(idc, ok ? block_of(i) : 0);
     const int bytes = ok ? (int)(kTileElems * 2) : 0;
     load_chunks(T.k, kbase + id * blk_stride, lane_off, bytes);
     load_chunks(T.v, vbase + id * blk_stride, lane_off, bytes);
   };
   auto run = [&](const MfmaTile& T, int i) {
-    const int t0 = start + i * 16;
+    const int t0 = start + block_of(i) * 16;
     const int valid = min(16, end - t0);
-    lds_u8_t* vb = vbufs[flip];
+    lds_u8_t* vb = stages[flip];
     flip ^= 1;
-    int lim[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) lim[t] = min(valid, max(ctx[t] - t0, 0));
+    const int lim[1] = {min(valid, max(ctx - t0, 0))};
     if (valid == 16 && min_ctx - t0 >= 16)
-      process_tile<false, NT>(S, T, qb, vb, 16, lim, q, n, p.scale_log2);
+      process_tile<false, 1>(S, T, qb, vb, 16, lim, q, n, p.scale_log2);
     else
-      process_tile<true, NT>(S, T, qb, vb, valid, lim, q, n, p.scale_log2);
+      process_tile<true, 1>(S, T, qb, vb, valid, lim, q, n, p.scale_log2);
   };
 
-  MfmaTile T[kPrefixNbuf];
-  int ld = 0, i = 0;
+  int i = wave;
+  if (i < nblk) {
+    MfmaTile T[kNbuf];
+    int ld = i;
 #pragma unroll
-  for (int s = 0; s < kPrefixNbuf - 1; ++s) load(T[s], ld++);
-  bool done = false;
-  while (!done) {
+    for (int s = 0; s < kNbuf - 1; ++s) {
+      load(T[s], ld);
+      ld += kWaves;
+    }
+    bool done = false;
+    while (!done) {
 #pragma unroll
-    for (int s = 0; s < kPrefixNbuf; ++s) {
-      if (!done) {
-        load(T[(s + kPrefixNbuf - 1) % kPrefixNbuf], ld++);
-        run(T[s], i);
-        ++i;
-        done = i >= nblk;
+      for (int s = 0; s < kNbuf; ++s) {
+        if (!done) {
+          load(T[(s + kNbuf - 1) % kNbuf], ld);
+          ld += kWaves;
+          run(T[s], i);
+          i += kWaves;
+          done = i >= nblk;
+        }
       }
     }
   }
 
-  // Normalise per row and write this partition's partials.
+  // Merge the waves through LDS (the staging area is free now): wave w
+  // then finishes rows 4w .. 4w+3 of the tile, lane l dims 2l, 2l+1.
+  const float lcol = group_sum4(S.l[0]);
+  __syncthreads();
+  lds_f32_t* sm = reinterpret_cast<lds_f32_t*>(smem);          // [W][16]
+  lds_f32_t* sl = sm + kWaves * 16;                             // [W][16]
+  lds_f32_t* sacc = sl + kWaves * 16;                           // [W][16][128]
+  if (q == 0) { sm[wave * 16 + n] = S.m[0]; sl[wave * 16 + n] = lcol; }
 #pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    const float lrow = group_sum4(S.l[t]);
-    const float inv = lrow > 0.f ? 1.0f / lrow : 0.f;
-    const int R = row0 + 16 * t + n;
-    if (q == 0 && col_ok[t]) {
-      const size_t row = ((size_t)(R / G) * p.num_q_heads + g * G + R % G) * p.part_stride + part;
-      p.part_lse[row] = lrow > 0.f ? (S.m[t] + log2f(lrow)) * kLn2 : -__builtin_inff();
+  for (int blk = 0; blk < 8; ++blk)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sacc[(wave * 16 + 4 * q + r) * kD + 16 * blk + n] = S.o[0][blk][r];
+  __syncthreads();
+
+#pragma unroll
+  for (int rr = 0; rr < 4; ++rr) {
+    const int r = 4 * wave + rr;
+    const int R = row0 + r;
+    if (R >= total_rows) break;
+    float mx = sm[r];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) mx = fmaxf(mx, sm[w * 16 + r]);
+    const float mref = (mx == -__builtin_inff()) ? 0.f : mx;
+    float lt = 0.f, o0 = 0.f, o1 = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float f = fast_exp2(sm[w * 16 + r] - mref);
+      lt = fmaf(sl[w * 16 + r], f, lt);
+      o0 = fmaf(sacc[(w * 16 + r) * kD + 2 * lane], f, o0);
+      o1 = fmaf(sacc[(w * 16 + r) * kD + 2 * lane + 1], f, o1);
     }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int Rr = row0 + 16 * t + 4 * q + r;
-      const float f = column_value(inv, q, r);
-      if (Rr < total_rows) {
-        const size_t row = ((size_t)(Rr / G) * p.num_q_heads + g * G + Rr % G) * p.part_stride + part;
-        float* po = p.part_o + row * kD + n;
-#pragma unroll
-        for (int blk = 0; blk < 8; ++blk) po[16 * blk] = S.o[t][blk][r] * f;
-      }
-    }
+    const float inv = lt > 0.f ? 1.0f / lt : 0.f;
+    const size_t row = ((size_t)(R / G) * p.num_q_heads + g * G + R % G) * p.part_stride + part;
+    *reinterpret_cast<float2*>(p.part_o + row * kD + 2 * lane) = make_float2(o0 * inv, o1 * inv);
+    if (lane == 0) p.part_lse[row] = lt > 0.f ? (mx + log2f(lt)) * kLn2 : -__builtin_inff();
   }
 }
 
