@@ -1,9 +1,12 @@
-// One-launch shared-prefix (cascade) step: the first `prefix_wgs` workgroups
-// run the shared-prefix pass (matrix-core tiles over all query rows), the
-// rest run the per-sequence decode over the tokens after the prefix.  Both
-// halves write disjoint (o, lse) partials, so they need no synchronisation;
-// running them in one grid lets the latency-bound prefix work overlap the
-// bandwidth-bound per-sequence work instead of preceding it.
+// One-launch shared-prefix (cascade) step: some workgroups run the
+// shared-prefix pass (matrix-core tiles over all query rows), the others run
+// the per-sequence decode over the tokens after the prefix.  Both write
+// disjoint (o, lse) partials, so they need no synchronisation.  The two kinds
+// alternate in runs of num_kv_heads workgroups, so every CU holds some of
+// each at once: the L2-fed prefix work overlaps the HBM-fed per-sequence work
+// instead of preceding it, and workgroup i still serves KV head
+// i % num_kv_heads, which keeps each head on one XCD (the dispatcher deals
+// workgroups to the XCDs round-robin).
 #include "mfma_body.h"
 #include "valu_body.h"
 
@@ -19,16 +22,31 @@ static_assert(PA_VALU_WAVES == mfma::kWaves, "both halves use the same workgroup
 
 template <int G>
 __global__ void __launch_bounds__(64 * mfma::kWaves) __attribute__((amdgpu_waves_per_eu(2, 8)))
-cascade_kernel(const PrefixParams pp, const DecodeParams dp, int prefix_wgs) {
+cascade_kernel(const PrefixParams pp, const DecodeParams dp, int prefix_runs, int decode_runs) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kCascadeLds];
   lds_u8_t* lds = (lds_u8_t*)smem;
-  const int wg = blockIdx.x;
-  if (wg < prefix_wgs) {
+  // Run r = blockIdx / Hkv: while both kinds remain, even runs are prefix
+  // runs and odd runs decode runs; then the longer kind continues alone.
+  const int hkv = dp.num_kv_heads;
+  const int run = blockIdx.x / hkv;
+  const int g = blockIdx.x - run * hkv;
+  const int both = min(prefix_runs, decode_runs);
+  bool prefix;
+  int idx;
+  if (run < 2 * both) {
+    prefix = (run & 1) == 0;
+    idx = run >> 1;
+  } else {
+    prefix = prefix_runs > decode_runs;
+    idx = both + (run - 2 * both);
+  }
+  const int wg = idx * hkv + g;
+  if (prefix) {
     mfma::prefix_mfma_body<G>(pp, wg, lds);
   } else if constexpr (G == 4) {
-    valu::decode_valu_body<128, 4, PA_VALU_WAVES, PA_VALU_NBUF, false>(dp, wg - prefix_wgs, lds);
+    valu::decode_valu_body<128, 4, PA_VALU_WAVES, PA_VALU_NBUF, false>(dp, wg, lds);
   } else {
-    mfma::decode_mfma_body<false>(dp, wg - prefix_wgs, lds);
+    mfma::decode_mfma_body<false>(dp, wg, lds);
   }
 }
 
@@ -38,17 +56,20 @@ hipError_t launch_cascade(const PrefixParams& pp, const DecodeParams& dp, int gr
                           hipStream_t stream) {
   const int64_t rows = (int64_t)pp.batch * group;
   const int64_t row_groups = (rows + mfma::kPrefixRowsPerWg - 1) / mfma::kPrefixRowsPerWg;
-  const int64_t prefix_wgs = (int64_t)pp.prefix_parts * row_groups * pp.num_kv_heads;
-  const int64_t decode_wgs = (int64_t)dp.num_parts * dp.batch * dp.num_kv_heads;
-  const int64_t grid = prefix_wgs + decode_wgs;
+  // Both grids are whole runs of num_kv_heads workgroups (the KV head is the
+  // fastest index of both).
+  if (pp.num_kv_heads != dp.num_kv_heads) return hipErrorInvalidValue;
+  const int64_t prefix_runs = (int64_t)pp.prefix_parts * row_groups;
+  const int64_t decode_runs = (int64_t)dp.num_parts * dp.batch;
+  const int64_t grid = (prefix_runs + decode_runs) * dp.num_kv_heads;
   if (grid == 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
   if (group == 4)
     hipLaunchKernelGGL(cascade_kernel<4>, dim3((unsigned)grid), dim3(64 * mfma::kWaves), 0, stream,
-                       pp, dp, (int)prefix_wgs);
+                       pp, dp, (int)prefix_runs, (int)decode_runs);
   else if (group == 8)
     hipLaunchKernelGGL(cascade_kernel<8>, dim3((unsigned)grid), dim3(64 * mfma::kWaves), 0, stream,
-                       pp, dp, (int)prefix_wgs);
+                       pp, dp, (int)prefix_runs, (int)decode_runs);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -19,10 +19,13 @@
 //    its dims; a DPP reduce-scatter across the 16 lanes of the row (ror 8,
 //    half-mirror, quad xor 2, quad xor 1) leaves in lane (J, c) the score of
 //    query row c/4 (+4k) for token 4(c%4)+J.
-//  * PV: lane (J, c) accumulates its dims over tokens = J mod 4; the
-//    probability of token 4u+J for row r sits in the same row group, at
-//    position 4(r%4)+u, so one DPP row broadcast delivers it.  The four row
-//    groups are summed once, at the end.
+//  * PV: lane (J, c) accumulates its dims over tokens = J mod 4, two tokens
+//    per v_dot2c_f32_bf16: probabilities are rounded to bf16 (the row sum adds
+//    the same rounded values, so the weights stay an exact convex combination)
+//    and packed in pairs (tokens 4u+J, 4(u+1)+J); one v_perm_b32 pairs the V
+//    values of those tokens for one dim.  The packed probabilities of row r
+//    sit in the same row group, at position 4(r%4)+u, so one DPP row
+//    broadcast delivers them.  The four row groups are summed once, at the end.
 //
 // The online softmax runs in log2 units (scores times scale*log2 e, hardware
 // exp2) and rescales the accumulator only when a block raises a row max by
@@ -150,33 +153,36 @@ __device__ __forceinline__ void process_tile(WaveState<D, G>& S, const KvTile<D>
     });
   }
 
-  float pr[R];
+  // Probabilities rounded to bf16; lanes with c even then hold the packed
+  // pair (token 4(c%4)+J, token 4(c%4+1)+J) of their row.
+  float pk[R];
 #pragma unroll
   for (int k = 0; k < R; ++k) {
     const float mref = S.m[k] == -__builtin_inff() ? 0.f : S.m[k];
-    pr[k] = fast_exp2(sc[k] - mref);
-    S.l[k] += pr[k];
+    const uint32_t pb = bf16_rne(fast_exp2(sc[k] - mref)) << 16;
+    S.l[k] += __uint_as_float(pb);
+    const uint32_t nb = __float_as_uint(dpp<kDppQuadXor1>(__uint_as_float(pb)));
+    pk[k] = __uint_as_float(__builtin_amdgcn_perm(nb, pb, 0x07060302u));  // lo: own, hi: c+1
   }
 
-  // PV: step u covers tokens 4u + J; row r's probability is at position
-  // 4(r%4) + u of slot r/4 in the same row group.
-  static_for<0, 4>([&](auto uc) {
-    constexpr int u = decltype(uc)::value;
-    float v[DPL];
+  // PV: step h covers tokens 4(2h)+J and 4(2h+1)+J; row r's packed pair is at
+  // position 4(r%4) + 2h of slot r/4 in the same row group.
+  static_for<0, 2>([&](auto hc) {
+    constexpr int h = decltype(hc)::value;
+    uint32_t vp[DPL];  // (token 2h, token 2h+1) bf16 pairs, one per dim
 #pragma unroll
     for (int w = 0; w < VW; ++w) {
-      v[2 * w] = bf16_lo(T.v[u][w]);
-      v[2 * w + 1] = bf16_hi(T.v[u][w]);
-    }
-    if (TAIL && 4 * u + grp >= valid) {
-#pragma unroll
-      for (int d = 0; d < DPL; ++d) v[d] = 0.f;
+      uint32_t a = T.v[2 * h][w], b = T.v[2 * h + 1][w];
+      if (TAIL && 4 * (2 * h) + grp >= valid) a = 0u;
+      if (TAIL && 4 * (2 * h + 1) + grp >= valid) b = 0u;
+      vp[2 * w] = __builtin_amdgcn_perm(b, a, 0x05040100u);      // dim 2w of both tokens
+      vp[2 * w + 1] = __builtin_amdgcn_perm(b, a, 0x07060302u);  // dim 2w+1
     }
     static_for<0, G>([&](auto rc) {
       constexpr int r = decltype(rc)::value;
-      const float pb = row_bcast<4 * (r % 4) + u>(pr[r / 4]);
+      const uint32_t pp = __float_as_uint(row_bcast<4 * (r % 4) + 2 * h>(pk[r / 4]));
 #pragma unroll
-      for (int d = 0; d < DPL; ++d) S.acc[r][d] = fmaf(pb, v[d], S.acc[r][d]);
+      for (int d = 0; d < DPL; ++d) S.acc[r][d] = dot2_bf16(pp, vp[d], S.acc[r][d]);
     });
   });
 }

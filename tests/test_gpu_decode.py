@@ -140,7 +140,11 @@ def test_split_partials_match_oracle():
         pbn = -(-int(n) // 64)
         rep = compare(o[b, :, :pbn], ro[b, :, :pbn], gpu_is_bf16_bits=False)
         assert rep.passed, rep
-        np.testing.assert_allclose(l[b, :, :pbn], rl[b, :, :pbn], rtol=0, atol=2e-4)
+        # Both kernels round each softmax weight to bf16 (RNE, relative error
+        # <= 2^-9) before the PV product and sum the rounded weights, so the
+        # partition's log-sum-exp is within log(1 + 2^-9) < 2^-9 of the exact
+        # value, plus fp32 accumulation error.
+        np.testing.assert_allclose(l[b, :, :pbn], rl[b, :, :pbn], rtol=0, atol=2 ** -9 + 1e-5)
 
 
 # ---------------------------------------------------------- bit-exact tests
