@@ -116,6 +116,13 @@ int validate_decode(const DecodeArgs& a, int32_t* group, const char* fn) {
   return PA_OK;
 }
 
+// Workgroup order of a decode grid.  With many partitions per sequence the
+// partitions of one sequence are dispatched together, so the end of the grid
+// is a mix of sequences instead of the last partitions of the longest ones
+// (measured: +3% on contexts of 8k-32k tokens in 512- or 1024-token
+// partitions, while partition-major is faster for a few partitions).
+int32_t item_order_for(int32_t num_parts) { return num_parts >= 16 ? 1 : 0; }
+
 pa::DecodeParams decode_params(const DecodeArgs& a) {
   pa::DecodeParams p{};
   p.k_pool = a.pool->k;
@@ -180,6 +187,7 @@ int decode_impl(const DecodeArgs& a, int32_t partition_size, void* out, float* p
   p.trace = trace;
   p.part_tokens = pl.part_tokens;
   p.num_parts = pl.num_parts;
+  p.item_order = item_order_for(pl.num_parts);
   p.token_offset = 0;
   p.part_offset = 0;
   p.part_stride = pl.num_parts;
@@ -470,6 +478,7 @@ int paged_attn_decode_cascade(const pa_kv_pool* pool, const void* q, const int32
   p.part_lse = partial_lse;
   p.part_tokens = cp.suf_tokens;
   p.num_parts = cp.suf_parts;
+  p.item_order = item_order_for(cp.suf_parts);
   p.token_offset = prefix_len;
   p.part_offset = cp.pre_parts;
   p.part_stride = cp.stride;

@@ -30,8 +30,26 @@ struct DecodeParams {
   int32_t part_stride;           // partitions per (sequence, head) in the partial buffers
   int32_t write_partials;        // 1: write (o, lse) partials; 0: write the bf16 output
   int32_t trace_tiles;           // trace slots per work item
+  int32_t item_order;            // workgroup -> work item order (decode_item)
   float scale_log2;              // softmax scale * log2(e)
 };
+
+// Work item (KV head g, sequence b, partition part) of decode workgroup wg.
+// The KV head varies fastest, so consecutive workgroups, which the
+// dispatcher deals to the XCDs round-robin, keep one KV head per XCD.  Then
+// either all sequences' partition 0, then partition 1, ... (item_order 0), or
+// all partitions of sequence 0, then sequence 1, ... (item_order 1).
+__device__ __forceinline__ void decode_item(const DecodeParams& p, int wg, int& g, int& b, int& part) {
+  g = wg % p.num_kv_heads;
+  wg /= p.num_kv_heads;
+  if (p.item_order == 0) {
+    b = wg % p.batch;
+    part = wg / p.batch;
+  } else {
+    part = wg % p.num_parts;
+    b = wg / p.num_parts;
+  }
+}
 
 // Attention of every query row of the batch over a prefix that all
 // sequences share (same physical blocks, read from sequence 0's table).

@@ -205,13 +205,8 @@ __device__ __forceinline__ void decode_valu_body(const DecodeParams& p, int wg_i
   const int grp = lane >> 4;
   const int tok = lane & 15;
 
-  // Work item; the KV head varies fastest so consecutive workgroups, which
-  // the dispatcher spreads over the XCDs round-robin, keep one KV head per XCD.
-  int wg = wg_index;
-  const int g = wg % p.num_kv_heads;
-  wg /= p.num_kv_heads;
-  const int b = wg % p.batch;
-  const int part = wg / p.batch;
+  int g, b, part;
+  decode_item(p, wg_index, g, b, part);
 
   const int start = p.token_offset + part * p.part_tokens;
   const int j0 = start >> 4;
