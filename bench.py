@@ -1,18 +1,21 @@
 """Benchmark of one decode step of paged decode attention on one MI355X.
 
 A step is one pass of the whole hot path over one batch: the split-KV decode
-kernel followed by the cross-split reduce, for every sequence and head of the
-batch.  The default workload is the SQL-generator stage (batch 64, 32 query /
-8 KV heads, head_dim 128, a 2048-token schema prefix shared by every
-sequence plus a unique 64..512-token suffix, 16-token blocks, 512-token
-partitions), with seeded synthetic bf16 N(0,1) inputs.
+(for batches that share a schema prefix, the one-launch cascade: a
+matrix-core pass over the shared prefix for all query rows plus the
+per-sequence decode of the tokens after it) followed by the cross-split
+reduce, for every sequence and head of the batch.  The default workload is
+the SQL-generator stage (batch 64, 32 query / 8 KV heads, head_dim 128, a
+2048-token schema prefix shared by every sequence plus a unique 64..512-token
+suffix, 16-token blocks), with seeded synthetic bf16 N(0,1) inputs.
 
 Timing: the pools and queries are replicated R times in HBM (R copies of the
 same data at different addresses, like R layers of a model) and consecutive
 steps rotate through them, so a step does not find its working set in the
 256 MB Infinity Cache left over from the previous step.  W warmup steps,
 then K timed steps bracketed by device synchronisation; per-kernel durations
-come from HIP events recorded around every launch on the launch stream.
+come from HIP events around K back-to-back launches of each kernel on the
+launch stream.
 
 Output: exactly one JSON line on stdout.  `value` is KV GB/s counting the
 algorithmic bytes of a step (each distinct cached token slot once, plus
@@ -51,8 +54,9 @@ DEFAULT_PARTITION = {1: 512, 2: 512, 3: 1024, 4: 1024, 5: 512}
 
 
 def default_prefix_partition(prefix_len: int) -> int:
-    """Prefix partition: a quarter of the shared prefix, within [256, 1024] tokens."""
-    return max(256, min(1024, (prefix_len // 4) // 16 * 16))
+    """Prefix partition: 1024 tokens (the library's maximum), or the whole prefix
+    when shorter; measured fastest on every stage workload with a prefix."""
+    return max(16, min(1024, -(-prefix_len // 16) * 16))
 
 
 def decode_kernel_of(w, prefix_len: int = 0) -> str:
@@ -229,7 +233,7 @@ def main():
     ap.add_argument("--cascade", choices=["auto", "on", "off"], default="auto",
                     help="shared-prefix cascade (auto: on when the batch shares a prefix)")
     ap.add_argument("--prefix-partition-size", type=int, default=None,
-                    help="tokens per prefix partition (default: a quarter of the prefix, 256..1024)")
+                    help="tokens per prefix partition (default: min(1024, prefix length))")
     ap.add_argument("--graph", action="store_true",
                     help="replay each step from a captured HIP graph (one per replica)")
     ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
