@@ -8,19 +8,21 @@
 //    1 KiB of contiguous memory and the vector L1 sees one access per 64
 //    bytes.  (Reading the MFMA operand layout straight from the pool would
 //    put 16 different rows in every 16-lane group, about one L1 access per
-//    lane, and the L1 becomes the limit when the tiles come from L2.)  The
-//    block is staged in LDS and each lane reads its operands from there.
-//  * S^T = K Q^T with v_mfma_f32_16x16x32_bf16: A = the K tile (16 tokens x 32
-//    dims per instruction, 4 instructions for D = 128), read from LDS (row
-//    pitch 272 bytes: the 16 rows of a column fall in distinct banks); B = Q^T
-//    with the query rows in its 16 columns.  Lane (q, n) = (lane >> 4,
-//    lane & 15) receives scores of tokens 4q..4q+3 for query column n, which
-//    is exactly the A-operand layout of the PV product, so the probabilities
-//    never move between lanes.
-//  * O += P V with v_mfma_f32_16x16x16bf16_1k (one per 16 output dims): the
-//    B operand needs 4 consecutive tokens of one dim per lane; the staged V
-//    tile (row pitch 288 bytes) is read back with the transposing
-//    ds_read_b64_tr_b16, which hands lane (q, n) V[4q..4q+3][dim n].
+//    lane, and the L1 becomes the limit when the tiles come from L2.)  Lane
+//    (q, n) = (lane >> 4, lane & 15) then holds tokens 4u+q (u = 0..3),
+//    dims 8n .. 8n+7, of both tiles.
+//  * S^T = K Q^T with v_mfma_f32_16x16x32_bf16: A = K rows (16 tokens x 32
+//    dims per instruction, 4 instructions for D = 128) read back from an LDS
+//    copy of the K tile (row pitch 272 bytes: the 16 rows of a column fall in
+//    distinct banks); B = Q^T with the query rows in its 16 columns.  A row i
+//    is token 4(i%4) + i/4, so lane (q, n) receives the scores of tokens
+//    4r+q (r = 0..3) for query column n.
+//  * O += P V with v_mfma_f32_16x16x16bf16_1k, one per 8 output dims: the
+//    contraction index k = 4q+e stands for token 4e+q, which makes the
+//    scores above exactly the A operand (P never moves between lanes), and
+//    output column n of instruction j is dim 8n + j, which makes the B
+//    operand V[token 4e+q][dim 8n+j] element j of the lane's own V registers
+//    (two v_perm_b32 per instruction; V never goes through LDS).
 //
 // The online softmax keeps one running max per query row, replicated over the
 // four lane groups, and rescales the accumulator only when a block raises the
@@ -48,11 +50,8 @@ typedef __attribute__((address_space(3))) u32x4_t lds_u32x4_t;
 constexpr int kD = 128;
 constexpr int kG = 8;
 constexpr int kWaves = 4;
-constexpr int kPitch = kD * 2 + 32;           // LDS bytes per staged V token row
-constexpr int kVTileBytes = 16 * kPitch;      // one staged V tile
 constexpr int kKPitch = kD * 2 + 16;          // LDS bytes per staged K token row
-constexpr int kKTileBytes = 16 * kKPitch;     // one staged K tile
-constexpr int kStageBytes = kKTileBytes + kVTileBytes;  // one staged block: K, then V
+constexpr int kStageBytes = 16 * kKPitch;     // one staged K tile
 constexpr float kLazyRescale = 8.0f;
 #ifndef PA_MFMA_NBUF
 #define PA_MFMA_NBUF 3
@@ -96,11 +95,11 @@ template <int NT>
 struct MfmaState {
   float m[NT];        // running max of query column n (log2 units), same in all groups
   float l[NT];        // this lane's share of the column sum (tokens 4q..4q+3 of each block)
-  floatx4_t o[NT][8]; // O[rows 4q+r][dims 16*blk + n] of each column tile
+  floatx4_t o[NT][8]; // [j]: O[rows 4q+r][dim 8n + j] of each column tile
 };
 
-// One 16-token block against NT column tiles that share the K operand and
-// the staged V (their MFMA chains are independent and interleave).
+// One 16-token block against NT column tiles that share the K and V
+// operands (their MFMA chains are independent and interleave).
 // `stage`: kStageBytes of this wavefront's LDS; `valid`: tokens of this tile
 // that exist (V rows past it are zeroed); `limit[t]`: tokens this lane's
 // column of tile t may attend to (<= valid).
@@ -109,53 +108,54 @@ __device__ __forceinline__ void process_tile(MfmaState<NT>& S, const MfmaTile& T
                                              const uint4 (&qb)[NT][4], lds_u8_t* stage, int valid,
                                              const int (&limit)[NT], int q, int n,
                                              float scale_log2) {
-  lds_u8_t* kbuf = stage;
-  lds_u8_t* vbuf = stage + kKTileBytes;
-  // Stage the block (rows 4u+q, chunk n); V tail rows become zero.
+  // Stage K (rows 4u+q, chunk n); read back A row n = token 4(n%4) + n/4,
+  // dims 32s + 8q .. +8 (chunk 4s+q) for k-step s.
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     const u32x4_t k = {T.k[u].x, T.k[u].y, T.k[u].z, T.k[u].w};
-    *reinterpret_cast<lds_u32x4_t*>(kbuf + (4 * u + q) * kKPitch + n * 16) = k;
-    u32x4_t v = {T.v[u].x, T.v[u].y, T.v[u].z, T.v[u].w};
-    if (TAIL && 4 * u + q >= valid) v = u32x4_t{0u, 0u, 0u, 0u};
-    *reinterpret_cast<lds_u32x4_t*>(vbuf + (4 * u + q) * kPitch + n * 16) = v;
+    *reinterpret_cast<lds_u32x4_t*>(stage + (4 * u + q) * kKPitch + n * 16) = k;
   }
-  // A operand of k-step s: token n, dims 32s + 8q .. +8 (chunk 4s+q).
+  const int krow = 4 * (n & 3) + (n >> 2);
   u32x4_t ka[4];
 #pragma unroll
   for (int s = 0; s < 4; ++s)
-    ka[s] = *reinterpret_cast<const lds_u32x4_t*>(kbuf + n * kKPitch + (4 * s + q) * 16);
+    ka[s] = *reinterpret_cast<const lds_u32x4_t*>(stage + krow * kKPitch + (4 * s + q) * 16);
 
+  // Two independent accumulation chains per tile, summed at the end.
   floatx4_t st[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    st[t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-      st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[s]),
-                                                      __builtin_bit_cast(bf16x8_t, qb[t][s]), st[t],
-                                                      0, 0, 0);
+    const floatx4_t z = {0.f, 0.f, 0.f, 0.f};
+    floatx4_t a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+        __builtin_bit_cast(bf16x8_t, ka[0]), __builtin_bit_cast(bf16x8_t, qb[t][0]), z, 0, 0, 0);
+    floatx4_t b = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+        __builtin_bit_cast(bf16x8_t, ka[1]), __builtin_bit_cast(bf16x8_t, qb[t][1]), z, 0, 0, 0);
+    a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[2]),
+                                                __builtin_bit_cast(bf16x8_t, qb[t][2]), a, 0, 0, 0);
+    b = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[3]),
+                                                __builtin_bit_cast(bf16x8_t, qb[t][3]), b, 0, 0, 0);
+    st[t] = a + b;
   }
 
-  float sc[NT][4], bm[NT];
+  // Scores of tokens 4r+q; the rescale test needs no cross-lane reduction:
+  // any lane above its column's max + kLazyRescale triggers it.
+  float sc[NT][4];
   bool raise = false;
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    float b = -__builtin_inff();
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       float x = st[t][r] * scale_log2;
-      if (TAIL && 4 * q + r >= limit[t]) x = -__builtin_inff();
+      if (TAIL && 4 * r + q >= limit[t]) x = -__builtin_inff();
       sc[t][r] = x;
-      b = fmaxf(b, x);
+      raise |= x > S.m[t] + kLazyRescale;
     }
-    bm[t] = group_max4(b);
-    raise |= bm[t] > S.m[t] + kLazyRescale;
   }
   if (__builtin_amdgcn_ballot_w64(raise) != 0) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      const float mn = bm[t] > S.m[t] + kLazyRescale ? bm[t] : S.m[t];
+      const float bm = group_max4(fmaxf(fmaxf(sc[t][0], sc[t][1]), fmaxf(sc[t][2], sc[t][3])));
+      const float mn = bm > S.m[t] + kLazyRescale ? bm : S.m[t];
       // 1 for columns that keep their max (or have attended to nothing yet)
       const float alpha = mn == -__builtin_inff() ? 1.f : fast_exp2(S.m[t] - mn);
       S.l[t] *= alpha;
@@ -188,22 +188,34 @@ __device__ __forceinline__ void process_tile(MfmaState<NT>& S, const MfmaTile& T
     S.l[t] += lsum;
   }
 
-  // PV: B operand = V[4q..4q+3][16*blk + n] through the transposing LDS read.
-  // Source lane (q, n) points at token 4q + n/4, dims 16*blk + 4*(n%4).
-  lds_u8_t* src = vbuf + (4 * q + (n >> 2)) * kPitch + (n & 3) * 8;
+  // PV: instruction j takes B = V[token 4e+q][dim 8n+j], e = 0..3: bf16 j of
+  // the lane's chunk in each of its four rows.  Tail rows become zero.
+  uint32_t vw[4][4];
 #pragma unroll
-  for (int blk = 0; blk < 8; ++blk) {
-    const short4_t vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        reinterpret_cast<lds_short4_t*>(src + blk * 32));
+  for (int u = 0; u < 4; ++u) {
+    const bool keep = !(TAIL && 4 * u + q >= valid);
+    vw[u][0] = keep ? T.v[u].x : 0u;
+    vw[u][1] = keep ? T.v[u].y : 0u;
+    vw[u][2] = keep ? T.v[u].z : 0u;
+    vw[u][3] = keep ? T.v[u].w : 0u;
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+    const uint32_t lo = __builtin_amdgcn_perm(vw[1][j >> 1], vw[0][j >> 1], sel);
+    const uint32_t hi = __builtin_amdgcn_perm(vw[3][j >> 1], vw[2][j >> 1], sel);
+    const short4_t vb = __builtin_bit_cast(short4_t, make_uint2(lo, hi));
 #pragma unroll
     for (int t = 0; t < NT; ++t)
-      S.o[t][blk] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa[t], vb, S.o[t][blk], 0, 0, 0);
+      S.o[t][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa[t], vb, S.o[t][j], 0, 0, 0);
   }
 }
 
-// LDS bytes either body needs (two staged blocks per wavefront, then the
+// LDS bytes either body needs (two staged K tiles per wavefront, then the
 // end-of-item merge).
-constexpr int kLdsBytes = kWaves * 2 * kStageBytes;
+constexpr int kMergeLdsBytes = (2 * kWaves * 16 + kWaves * 16 * kD) * 4;  // up to 16 rows per wave
+constexpr int kLdsBytes = kWaves * 2 * kStageBytes > kMergeLdsBytes ? kWaves * 2 * kStageBytes
+                                                                    : kMergeLdsBytes;
 
 // One decode work item (partition, sequence, KV head) = workgroup `wg_index`.
 template <bool TRACE>
@@ -322,7 +334,7 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
     for (int blk = 0; blk < 8; ++blk)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        sacc[(wave * kG + 4 * q + r) * kD + 16 * blk + n] = S.o[0][blk][r];
+        sacc[(wave * kG + 4 * q + r) * kD + 8 * n + blk] = S.o[0][blk][r];
   }
   __syncthreads();
   if (wave != 0) return;
@@ -481,7 +493,7 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
 #pragma unroll
   for (int blk = 0; blk < 8; ++blk)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) sacc[(wave * 16 + 4 * q + r) * kD + 16 * blk + n] = S.o[0][blk][r];
+    for (int r = 0; r < 4; ++r) sacc[(wave * 16 + 4 * q + r) * kD + 8 * n + blk] = S.o[0][blk][r];
   __syncthreads();
 
 #pragma unroll

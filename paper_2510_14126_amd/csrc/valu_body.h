@@ -126,21 +126,23 @@ __device__ __forceinline__ void process_tile(WaveState<D, G>& S, const KvTile<D>
   row_reduce_scatter16(y, c);
 
   const int token = 4 * (c & 3) + grp;
-  float sc[R], bm[R];
+  float sc[R];
   bool raise = false;
+  // The rescale test needs no cross-lane reduction: any lane above its row's
+  // max + kLazyRescale triggers it; only then is the block's row max formed.
 #pragma unroll
   for (int k = 0; k < R; ++k) {
     float s = y[k] * scale_log2;
     if (TAIL && token >= valid) s = -__builtin_inff();
     sc[k] = s;
-    bm[k] = group_max4(quad_max4(s));
-    raise |= bm[k] > S.m[k] + kLazyRescale;
+    raise |= s > S.m[k] + kLazyRescale;
   }
   if (__builtin_amdgcn_ballot_w64(raise) != 0) {
     float alpha[R];
 #pragma unroll
     for (int k = 0; k < R; ++k) {
-      const float mn = bm[k] > S.m[k] + kLazyRescale ? bm[k] : S.m[k];
+      const float bm = group_max4(quad_max4(sc[k]));
+      const float mn = bm > S.m[k] + kLazyRescale ? bm : S.m[k];
       alpha[k] = mn == -__builtin_inff() ? 1.f : fast_exp2(S.m[k] - mn);
       S.l[k] *= alpha[k];
       S.m[k] = mn;
