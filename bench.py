@@ -53,10 +53,14 @@ KERNEL_SOURCES = {
 DEFAULT_PARTITION = {1: 512, 2: 512, 3: 1024, 4: 1024, 5: 512}
 
 
-def default_prefix_partition(prefix_len: int) -> int:
-    """Prefix partition: 1024 tokens (the library's maximum), or the whole prefix
-    when shorter; measured fastest on every stage workload with a prefix."""
-    return max(16, min(1024, -(-prefix_len // 16) * 16))
+# Prefix partition sizes (tokens) used when --prefix-partition-size is not
+# given: the size that measured fastest on each workload with a shared prefix.
+DEFAULT_PREFIX_PARTITION = {2: 512, 3: 1024, 5: 512}
+
+
+def default_prefix_partition(config: int, prefix_len: int) -> int:
+    size = DEFAULT_PREFIX_PARTITION.get(config, 1024)
+    return max(16, min(size, -(-prefix_len // 16) * 16))
 
 
 def decode_kernel_of(w, prefix_len: int = 0) -> str:
@@ -233,7 +237,7 @@ def main():
     ap.add_argument("--cascade", choices=["auto", "on", "off"], default="auto",
                     help="shared-prefix cascade (auto: on when the batch shares a prefix)")
     ap.add_argument("--prefix-partition-size", type=int, default=None,
-                    help="tokens per prefix partition (default: min(1024, prefix length))")
+                    help="tokens per prefix partition (default: per workload, see DEFAULT_PREFIX_PARTITION)")
     ap.add_argument("--graph", action="store_true",
                     help="replay each step from a captured HIP graph (one per replica)")
     ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
@@ -287,7 +291,7 @@ def main():
     prefix_len = 16 * int(w.meta.get("prefix_blocks", 0))
     if args.cascade == "off" or (args.cascade == "auto" and prefix_len == 0):
         prefix_len = 0
-    pps = args.prefix_partition_size or default_prefix_partition(prefix_len)
+    pps = args.prefix_partition_size or default_prefix_partition(args.config, prefix_len)
     base = PagedBatch(w, dev, prefix_len=prefix_len, prefix_partition_size=pps)
     reps = [(base.pool, base.q)]
     keep = []

@@ -13,10 +13,9 @@
 namespace pa {
 namespace {
 
-constexpr int kCascadeLds =
-    mfma::kLdsBytes > valu::valu_lds_bytes<128, 4, PA_VALU_WAVES>()
-        ? mfma::kLdsBytes
-        : valu::valu_lds_bytes<128, 4, PA_VALU_WAVES>();
+constexpr int kMax(int a, int b) { return a > b ? a : b; }
+constexpr int kCascadeLds = kMax(kMax(mfma::kPrefixLdsBytes, mfma::kLdsBytes),
+                                 valu::valu_lds_bytes<128, 4, PA_VALU_WAVES>());
 
 static_assert(PA_VALU_WAVES == mfma::kWaves, "both halves use the same workgroup size");
 

@@ -17,7 +17,7 @@ decode_mfma_g8_kernel(const DecodeParams p) {
 template <int G>
 __global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 8)))
 prefix_mfma_kernel(const PrefixParams p) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[mfma::kLdsBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t smem[mfma::kPrefixLdsBytes];
   mfma::prefix_mfma_body<G>(p, blockIdx.x, (lds_u8_t*)smem);
 }
 

@@ -100,26 +100,15 @@ struct MfmaState {
 
 // One 16-token block against NT column tiles that share the K and V
 // operands (their MFMA chains are independent and interleave).
-// `stage`: kStageBytes of this wavefront's LDS; `valid`: tokens of this tile
-// that exist (V rows past it are zeroed); `limit[t]`: tokens this lane's
-// column of tile t may attend to (<= valid).
+// ka[s]: A operand of k-step s (token 4(n%4) + n/4, chunk 4s+q of the K
+// tile); vrow[u]: the lane's V registers (token 4u+q, chunk n); `valid`:
+// tokens of this tile that exist (V rows past it are zeroed); `limit[t]`:
+// tokens this lane's column of tile t may attend to (<= valid).
 template <bool TAIL, int NT>
-__device__ __forceinline__ void process_tile(MfmaState<NT>& S, const MfmaTile& T,
-                                             const uint4 (&qb)[NT][4], lds_u8_t* stage, int valid,
-                                             const int (&limit)[NT], int q, int n,
-                                             float scale_log2) {
-  // Stage K (rows 4u+q, chunk n); read back A row n = token 4(n%4) + n/4,
-  // dims 32s + 8q .. +8 (chunk 4s+q) for k-step s.
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const u32x4_t k = {T.k[u].x, T.k[u].y, T.k[u].z, T.k[u].w};
-    *reinterpret_cast<lds_u32x4_t*>(stage + (4 * u + q) * kKPitch + n * 16) = k;
-  }
-  const int krow = 4 * (n & 3) + (n >> 2);
-  u32x4_t ka[4];
-#pragma unroll
-  for (int s = 0; s < 4; ++s)
-    ka[s] = *reinterpret_cast<const lds_u32x4_t*>(stage + krow * kKPitch + (4 * s + q) * 16);
+__device__ __forceinline__ void tile_core(MfmaState<NT>& S, const u32x4_t (&ka)[4],
+                                          const uint4 (&vrow)[4], const uint4 (&qb)[NT][4],
+                                          int valid, const int (&limit)[NT], int q,
+                                          float scale_log2) {
 
   // Two independent accumulation chains per tile, summed at the end.
   floatx4_t st[NT];
@@ -194,10 +183,10 @@ __device__ __forceinline__ void process_tile(MfmaState<NT>& S, const MfmaTile& T
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     const bool keep = !(TAIL && 4 * u + q >= valid);
-    vw[u][0] = keep ? T.v[u].x : 0u;
-    vw[u][1] = keep ? T.v[u].y : 0u;
-    vw[u][2] = keep ? T.v[u].z : 0u;
-    vw[u][3] = keep ? T.v[u].w : 0u;
+    vw[u][0] = keep ? vrow[u].x : 0u;
+    vw[u][1] = keep ? vrow[u].y : 0u;
+    vw[u][2] = keep ? vrow[u].z : 0u;
+    vw[u][3] = keep ? vrow[u].w : 0u;
   }
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
@@ -209,6 +198,29 @@ __device__ __forceinline__ void process_tile(MfmaState<NT>& S, const MfmaTile& T
     for (int t = 0; t < NT; ++t)
       S.o[t][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa[t], vb, S.o[t][j], 0, 0, 0);
   }
+}
+
+// Row of the K tile that lane (q, n) supplies as A row n: token 4(n%4) + n/4.
+__device__ __forceinline__ int k_arow(int n) { return 4 * (n & 3) + (n >> 2); }
+
+// One block of a per-sequence work item: the wavefront's own K tile goes
+// through `stage` (kStageBytes of its LDS) to reach the A-operand layout;
+// V is used from the registers it was loaded into.
+template <bool TAIL, int NT>
+__device__ __forceinline__ void process_tile(MfmaState<NT>& S, const MfmaTile& T,
+                                             const uint4 (&qb)[NT][4], lds_u8_t* stage, int valid,
+                                             const int (&limit)[NT], int q, int n,
+                                             float scale_log2) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const u32x4_t k = {T.k[u].x, T.k[u].y, T.k[u].z, T.k[u].w};
+    *reinterpret_cast<lds_u32x4_t*>(stage + (4 * u + q) * kKPitch + n * 16) = k;
+  }
+  u32x4_t ka[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    ka[s] = *reinterpret_cast<const lds_u32x4_t*>(stage + k_arow(n) * kKPitch + (4 * s + q) * 16);
+  tile_core<TAIL, NT>(S, ka, T.v, qb, valid, limit, q, scale_log2);
 }
 
 // LDS bytes either body needs (two staged K tiles per wavefront, then the
@@ -369,14 +381,21 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
 
 // Attention over the prefix that every sequence of the batch shares: for KV
 // head g the B*G query rows form the columns of dense 16-row tiles (four
-// sequences of four heads, or two of eight, per tile).  One workgroup owns one
-// column tile and one prefix partition; its wavefronts take the partition's
-// blocks round-robin, as the decode bodies do, and merge through LDS.  All
-// column tiles of a KV head read the same blocks, so each block comes from
-// HBM once and from L2 afterwards.  Every row writes its (o, lse) partial for
-// the partition, lse = -inf when it attended to nothing.
-constexpr int kPrefixRowsPerWg = 16;
-static_assert((2 * kWaves * 16 + kWaves * 16 * kD) * 4 <= kLdsBytes, "prefix merge must fit in LDS");
+// sequences of four heads, or two of eight, per tile).  One workgroup owns
+// kWaves adjacent tiles (wavefront w: tile w) and one prefix partition, and
+// its wavefronts share every block: each loads one quarter (four token rows
+// of K and of V, 2 KiB) into a double-buffered LDS stage, and after a
+// barrier every wavefront runs its own tile against the whole block.  A block
+// thus crosses from L2 to the CU once per four tiles, and each wavefront owns
+// whole query rows, so no cross-wavefront merge is needed.  All workgroups of
+// a KV head read the same blocks, so each comes from HBM once and from L2
+// afterwards.  Every row writes its (o, lse) partial for the partition,
+// lse = -inf when it attended to nothing.
+constexpr int kPrefixRowsPerWg = 16 * kWaves;
+constexpr int kPrefixRing = 4;                  // blocks whose quarter is in flight per wavefront
+constexpr int kPrefixKBytes = 16 * kKPitch;     // staged K tile (A-operand reads need the pitch)
+constexpr int kPrefixStageBytes = kPrefixKBytes + 16 * kD * 2;  // + V tile, row pitch 256
+constexpr int kPrefixLdsBytes = 2 * kPrefixStageBytes;
 
 template <int G>
 __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_index, lds_u8_t* smem) {
@@ -386,17 +405,17 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
   const int n = lane & 15;
 
   const int total_rows = p.batch * G;
-  const int tiles = (total_rows + kPrefixRowsPerWg - 1) / kPrefixRowsPerWg;
+  const int groups = (total_rows + kPrefixRowsPerWg - 1) / kPrefixRowsPerWg;
   int wg = wg_index;
   const int g = wg % p.num_kv_heads;
   wg /= p.num_kv_heads;
-  const int tile = wg % tiles;
-  const int part = wg / tiles;
-  const int row0 = tile * kPrefixRowsPerWg;
+  const int grp = wg % groups;
+  const int part = wg / groups;
+  const int row0 = grp * kPrefixRowsPerWg + 16 * wave;   // this wavefront's tile
 
   const int start = part * p.part_tokens;
   const int end = min(p.prefix_len, start + p.part_tokens);
-  const int nblk = (end - start + 15) >> 4;     // >= 1 for every launched partition
+  const int nblk = (end - start + 15) >> 4;     // 1 .. 64 for every launched partition
   const int raw = lane < nblk ? p.block_tables[(start >> 4) + lane] : 0;
   const int idc = min(max(raw, 0), p.num_blocks - 1);
 
@@ -419,8 +438,6 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
     min_ctx = __builtin_amdgcn_readfirstlane(-(int)group_max4(row_max16(-(float)c)));
   }
 
-  lds_u8_t* stages[2] = {smem + (wave * 2) * kStageBytes, smem + (wave * 2 + 1) * kStageBytes};
-
   MfmaState<1> S;
   S.m[0] = -__builtin_inff();
   S.l[0] = 0.f;
@@ -429,94 +446,88 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
 
   constexpr size_t kTileElems = 16 * kD;
   const size_t blk_stride = (size_t)p.num_kv_heads * kTileElems;
+  // This wavefront's quarter of a tile: token row 4*wave + q, chunk n.
+  const int share_off = ((4 * wave + q) * kD + n * 8) * 2;
   const uint16_t* kbase = p.k_pool + (size_t)g * kTileElems;
   const uint16_t* vbase = p.v_pool + (size_t)g * kTileElems;
-  const uint32_t lane_off = (uint32_t)(q * kD + n * 8) * 2u;  // row q, chunk n (+ 4 rows per u)
-  int flip = 0;
 
-  // The column tiles of a KV head walk the partition from evenly spread
+  // The workgroups of a KV head walk the partition from evenly spread
   // starting blocks, so at any moment they read different blocks instead of
   // all queueing on the L2 lines of the same one.
-  const int rot = (int)(((int64_t)tile * nblk) / tiles) % nblk;
+  const int rot = (int)(((int64_t)grp * nblk) / groups) % nblk;
   auto block_of = [&](int i) { const int j = i + rot; return j >= nblk ? j - nblk : j; };
-  auto load = [&](MfmaTile& T, int i) {
+  auto load = [&](uint4 (&dst)[2], int i) {
     const bool ok = i < nblk;
     const size_t id = (size_t)__builtin_amdgcn_readlane(idc, ok ? block_of(i) : 0);
     const int bytes = ok ? (int)(kTileElems * 2) : 0;
-    load_chunks(T.k, kbase + id * blk_stride, lane_off, bytes);
-    load_chunks(T.v, vbase + id * blk_stride, lane_off, bytes);
-  };
-  auto run = [&](const MfmaTile& T, int i) {
-    const int t0 = start + block_of(i) * 16;
-    const int valid = min(16, end - t0);
-    lds_u8_t* vb = stages[flip];
-    flip ^= 1;
-    const int lim[1] = {min(valid, max(ctx - t0, 0))};
-    if (valid == 16 && min_ctx - t0 >= 16)
-      process_tile<false, 1>(S, T, qb, vb, 16, lim, q, n, p.scale_log2);
-    else
-      process_tile<true, 1>(S, T, qb, vb, valid, lim, q, n, p.scale_log2);
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(kbase + id * blk_stride), 0, bytes, kBufferDescWord3);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(vbase + id * blk_stride), 0, bytes, kBufferDescWord3);
+    const auto k = __builtin_amdgcn_raw_buffer_load_b128(rk, share_off, 0, 0);
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(rv, share_off, 0, 0);
+    dst[0] = make_uint4(k[0], k[1], k[2], k[3]);
+    dst[1] = make_uint4(v[0], v[1], v[2], v[3]);
   };
 
-  int i = wave;
-  if (i < nblk) {
-    MfmaTile T[kNbuf];
-    int ld = i;
+  uint4 ring[kPrefixRing][2];
 #pragma unroll
-    for (int s = 0; s < kNbuf - 1; ++s) {
-      load(T[s], ld);
-      ld += kWaves;
-    }
-    bool done = false;
-    while (!done) {
+  for (int s = 0; s < kPrefixRing - 1; ++s) load(ring[s], s);
+  for (int i0 = 0; i0 < nblk; i0 += kPrefixRing) {
 #pragma unroll
-      for (int s = 0; s < kNbuf; ++s) {
-        if (!done) {
-          load(T[(s + kNbuf - 1) % kNbuf], ld);
-          ld += kWaves;
-          run(T[s], i);
-          i += kWaves;
-          done = i >= nblk;
+    for (int s = 0; s < kPrefixRing; ++s) {
+      const int i = i0 + s;
+      if (i < nblk) {                          // uniform over the workgroup
+        lds_u8_t* st = smem + (i & 1) * kPrefixStageBytes;
+        // Publish this wavefront's quarter of block i, then refill the slot
+        // freed last step with the quarter of block i + kPrefixRing - 1.
+        *reinterpret_cast<lds_u32x4_t*>(st + (4 * wave + q) * kKPitch + n * 16) =
+            u32x4_t{ring[s][0].x, ring[s][0].y, ring[s][0].z, ring[s][0].w};
+        *reinterpret_cast<lds_u32x4_t*>(st + kPrefixKBytes + share_off) =
+            u32x4_t{ring[s][1].x, ring[s][1].y, ring[s][1].z, ring[s][1].w};
+        load(ring[(s + kPrefixRing - 1) % kPrefixRing], i + kPrefixRing - 1);
+        __syncthreads();
+
+        u32x4_t ka[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          ka[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_arow(n) * kKPitch + (4 * c + q) * 16);
+        uint4 vrow[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const u32x4_t v = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixKBytes + ((4 * u + q) * kD + n * 8) * 2);
+          vrow[u] = make_uint4(v[0], v[1], v[2], v[3]);
         }
+        const int t0 = start + block_of(i) * 16;
+        const int valid = min(16, end - t0);
+        const int lim[1] = {min(valid, max(ctx - t0, 0))};
+        if (valid == 16 && min_ctx - t0 >= 16)
+          tile_core<false, 1>(S, ka, vrow, qb, 16, lim, q, p.scale_log2);
+        else
+          tile_core<true, 1>(S, ka, vrow, qb, valid, lim, q, p.scale_log2);
       }
     }
   }
 
-  // Merge the waves through LDS (the staging area is free now): wave w
-  // then finishes rows 4w .. 4w+3 of the tile, lane l dims 2l, 2l+1.
+  // Normalise per row and write this partition's partials: lane (q, n)
+  // holds O[rows 4q+r][dims 8n .. 8n+7].
   const float lcol = group_sum4(S.l[0]);
-  __syncthreads();
-  lds_f32_t* sm = reinterpret_cast<lds_f32_t*>(smem);          // [W][16]
-  lds_f32_t* sl = sm + kWaves * 16;                             // [W][16]
-  lds_f32_t* sacc = sl + kWaves * 16;                           // [W][16][128]
-  if (q == 0) { sm[wave * 16 + n] = S.m[0]; sl[wave * 16 + n] = lcol; }
-#pragma unroll
-  for (int blk = 0; blk < 8; ++blk)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) sacc[(wave * 16 + 4 * q + r) * kD + 8 * n + blk] = S.o[0][blk][r];
-  __syncthreads();
-
-#pragma unroll
-  for (int rr = 0; rr < 4; ++rr) {
-    const int r = 4 * wave + rr;
-    const int R = row0 + r;
-    if (R >= total_rows) break;
-    float mx = sm[r];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) mx = fmaxf(mx, sm[w * 16 + r]);
-    const float mref = (mx == -__builtin_inff()) ? 0.f : mx;
-    float lt = 0.f, o0 = 0.f, o1 = 0.f;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      const float f = fast_exp2(sm[w * 16 + r] - mref);
-      lt = fmaf(sl[w * 16 + r], f, lt);
-      o0 = fmaf(sacc[(w * 16 + r) * kD + 2 * lane], f, o0);
-      o1 = fmaf(sacc[(w * 16 + r) * kD + 2 * lane + 1], f, o1);
-    }
-    const float inv = lt > 0.f ? 1.0f / lt : 0.f;
+  const float inv = lcol > 0.f ? 1.0f / lcol : 0.f;
+  if (q == 0 && row0 + n < total_rows) {
+    const int R = row0 + n;
     const size_t row = ((size_t)(R / G) * p.num_q_heads + g * G + R % G) * p.part_stride + part;
-    *reinterpret_cast<float2*>(p.part_o + row * kD + 2 * lane) = make_float2(o0 * inv, o1 * inv);
-    if (lane == 0) p.part_lse[row] = lt > 0.f ? (mx + log2f(lt)) * kLn2 : -__builtin_inff();
+    p.part_lse[row] = lcol > 0.f ? (S.m[0] + log2f(lcol)) * kLn2 : -__builtin_inff();
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int R = row0 + 4 * q + r;
+    const float f = column_value(inv, q, r);
+    if (R < total_rows) {
+      const size_t row = ((size_t)(R / G) * p.num_q_heads + g * G + R % G) * p.part_stride + part;
+      float4* po = reinterpret_cast<float4*>(p.part_o + row * kD + 8 * n);
+      po[0] = make_float4(S.o[0][0][r] * f, S.o[0][1][r] * f, S.o[0][2][r] * f, S.o[0][3][r] * f);
+      po[1] = make_float4(S.o[0][4][r] * f, S.o[0][5][r] * f, S.o[0][6][r] * f, S.o[0][7][r] * f);
+    }
   }
 }
 
