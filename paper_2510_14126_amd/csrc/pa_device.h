@@ -77,29 +77,28 @@ __device__ __forceinline__ float quad_sum4(float x) {
   return x + dpp<kDppQuadXor2>(x);
 }
 
-// One level of a reduce-scatter: each lane pairs with the lane CTRL maps it
-// to; the lane with `upper` set keeps the upper half of x[0..2H) and the other
-// the lower half, each adding its partner's copy of the half it keeps.
+// Reduce-scatter over the 16 lanes of each DPP row without lane-dependent
+// selects.  Every lane holds N partial values (N a multiple of 16) in slot
+// order s; slot s of lane c must hold index s XOR M(c), where M is the
+// GF(2)-linear map M(c) = b3 e3 + b2 (e2 + e1 + e0) + b1 e1 + b0 e0 on the
+// top four bits of the index (b_i = bit i of c, e_j = bit j of s * 16 / N).
+// Each level keeps the lower half of the slots and adds the partner's upper
+// half; the partners (c^8 by row_ror 8, c^7 by row_half_mirror, c^2, c^1)
+// hold the same indices there because M(partner flip) is exactly the bit the
+// level consumes.  Afterwards lane c holds in x[0 .. N/16) the row-wide sums
+// of indices M(c) * N/16 ...
 template <int CTRL, int H, int N>
-__device__ __forceinline__ void reduce_scatter_level(float (&x)[N], bool upper) {
+__device__ __forceinline__ void fold_level(float (&x)[N]) {
 #pragma unroll
-  for (int i = 0; i < H; ++i) {
-    const float send = upper ? x[i] : x[i + H];
-    const float keep = upper ? x[i + H] : x[i];
-    x[i] = keep + dpp<CTRL>(send);
-  }
+  for (int i = 0; i < H; ++i) x[i] = x[i] + dpp<CTRL>(x[i + H]);
 }
-
-// Reduce-scatter over the 16 lanes of each DPP row.  Every lane holds N
-// partial values (N a multiple of 16); afterwards lane c of a row holds in
-// x[0 .. N/16) the row-wide sums of values c*N/16 .. c*N/16 + N/16 - 1.
 template <int N>
-__device__ __forceinline__ void row_reduce_scatter16(float (&x)[N], int c) {
+__device__ __forceinline__ void row_reduce_scatter16(float (&x)[N]) {
   static_assert(N % 16 == 0, "N must be a multiple of 16");
-  reduce_scatter_level<kDppRowRor8, N / 2>(x, (c & 8) != 0);        // partner c ^ 8
-  reduce_scatter_level<kDppRowHalfMirror, N / 4>(x, (c & 4) != 0);  // partner (c & 8) | (7 - c % 8)
-  reduce_scatter_level<kDppQuadXor2, N / 8>(x, (c & 2) != 0);       // partner c ^ 2
-  reduce_scatter_level<kDppQuadXor1, N / 16>(x, (c & 1) != 0);      // partner c ^ 1
+  fold_level<kDppRowRor8, N / 2>(x);        // partner c ^ 8
+  fold_level<kDppRowHalfMirror, N / 4>(x);  // partner c ^ 7
+  fold_level<kDppQuadXor2, N / 8>(x);       // partner c ^ 2
+  fold_level<kDppQuadXor1, N / 16>(x);      // partner c ^ 1
 }
 
 // Max / sum over the 16 lanes of each row; every lane receives the result.

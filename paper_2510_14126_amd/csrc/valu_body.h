@@ -18,14 +18,18 @@
 //  * QK^T: each lane forms 4G partial dot products (v_dot2c_f32_bf16) over
 //    its dims; a DPP reduce-scatter across the 16 lanes of the row (ror 8,
 //    half-mirror, quad xor 2, quad xor 1) leaves in lane (J, c) the score of
-//    query row c/4 (+4k) for token 4(c%4)+J.
+//    query row c/4 (+4k) for token 4 tg(c) + J, tg(c) = (c%4) ^ 3*bit2(c).
+//    The reduce-scatter needs no lane-dependent selects: each lane loads its
+//    query rows and its K row quads in a lane-dependent order (row r ^ c/4,
+//    quad u ^ tg(c)), so every level keeps the same slots on both partners.
 //  * PV: lane (J, c) accumulates its dims over tokens = J mod 4, two tokens
 //    per v_dot2c_f32_bf16: probabilities are rounded to bf16 (the row sum adds
 //    the same rounded values, so the weights stay an exact convex combination)
-//    and packed in pairs (tokens 4u+J, 4(u+1)+J); one v_perm_b32 pairs the V
-//    values of those tokens for one dim.  The packed probabilities of row r
-//    sit in the same row group, at position 4(r%4)+u, so one DPP row
-//    broadcast delivers them.  The four row groups are summed once, at the end.
+//    and packed in pairs (tokens 4(2h)+J, 4(2h+1)+J) by the even lane of each
+//    lane pair; one v_perm_b32 pairs the V values of those tokens for one dim.
+//    The packed probabilities of row r sit in the same row group at a fixed
+//    position, so one DPP row broadcast delivers them.  The four row groups
+//    are summed once, at the end.
 //
 // The online softmax runs in log2 units (scores times scale*log2 e, hardware
 // exp2) and rescales the accumulator only when a block raises a row max by
@@ -66,24 +70,32 @@ __device__ __forceinline__ void static_for(F&& f) {
 template <int D>
 struct KvTile {
   static constexpr int VW = D / 32;   // dwords per lane per token (4: 16 B, 2: 8 B)
-  uint32_t k[4][VW];                  // token 4u + J, dims (D/16)*c ..
-  uint32_t v[4][VW];
+  uint32_t k[4][VW];                  // token 4(u ^ tg(c)) + J, dims (D/16)*c ..
+  uint32_t v[4][VW];                  // token 4u + J, dims (D/16)*c ..
 };
 
-// Rows 4u+J, dims (D/16)*c .. of one tile, through a buffer descriptor built
-// from the wave-uniform tile address (scalar registers) and the lane's fixed
-// byte offset inside a 4-token row quad: no per-tile vector address math, and
-// the descriptor bounds every access to the tile.
+// Token quad whose scores lane (J, c) holds after the reduce-scatter.
+__device__ __forceinline__ int token_quad(int c) { return (c & 3) ^ (3 * ((c >> 2) & 1)); }
+
+// Row-group position holding the packed probabilities of row r (mod 4) for
+// token quads 2h and 2h+1: the even lane of the two that own those quads.
+template <int R4, int H>
+constexpr int pair_pos() { return 4 * R4 + ((R4 & 1) ? 2 - 2 * H : 2 * H); }
+
+// Dims (D/16)*c .. of one token row per row quad u, through a buffer
+// descriptor built from the wave-uniform tile address (scalar registers) and
+// the lane's fixed byte offset lane_off[u] into the tile: no per-tile vector
+// address math, and the descriptor bounds every access to the tile.
 // `bytes` = 0 turns the loads into no-ops that return zeros but still count
 // as issued, so every path through the prefetch ring issues the same loads.
 template <int D>
 __device__ __forceinline__ void load_rows(uint32_t (&dst)[4][D / 32], const uint16_t* tile,
-                                          uint32_t lane_off, int bytes) {
+                                          const uint32_t (&lane_off)[4], int bytes) {
   const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(tile), 0, bytes, kBufferDescWord3);
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const int off = (int)lane_off + u * (4 * D * 2);
+    const int off = (int)lane_off[u];
     if constexpr (D == 128) {
       const auto x = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0);
       dst[u][0] = x[0]; dst[u][1] = x[1]; dst[u][2] = x[2]; dst[u][3] = x[3];
@@ -107,6 +119,7 @@ template <int D, int G, bool TAIL>
 __device__ __forceinline__ void process_tile(WaveState<D, G>& S, const KvTile<D>& T,
                                              const uint32_t (&qv)[G][D / 32], int valid,
                                              int grp, int c, float scale_log2) {
+  // (slot order of qv and T.k is lane-dependent; see row_reduce_scatter16)
   constexpr int R = G / 4;
   constexpr int VW = D / 32;
   constexpr int DPL = D / 16;
@@ -123,9 +136,9 @@ __device__ __forceinline__ void process_tile(WaveState<D, G>& S, const KvTile<D>
       for (int w = 0; w < VW; ++w) a = dot2_bf16(qv[r][w], T.k[u][w], a);
       y[R * (4 * (r % 4) + u) + r / 4] = a;
     }
-  row_reduce_scatter16(y, c);
+  row_reduce_scatter16(y);
 
-  const int token = 4 * (c & 3) + grp;
+  const int token = 4 * token_quad(c) + grp;
   float sc[R];
   bool raise = false;
   // The rescale test needs no cross-lane reduction: any lane above its row's
@@ -155,8 +168,10 @@ __device__ __forceinline__ void process_tile(WaveState<D, G>& S, const KvTile<D>
     });
   }
 
-  // Probabilities rounded to bf16; lanes with c even then hold the packed
-  // pair (token 4(c%4)+J, token 4(c%4+1)+J) of their row.
+  // Probabilities rounded to bf16; even lanes then hold the packed pair
+  // (even token quad, odd token quad) of their row: the lane's own quad is
+  // even unless bit 2 of c is set.
+  const uint32_t pack_sel = ((c >> 2) & 1) ? 0x03020706u : 0x07060302u;
   float pk[R];
 #pragma unroll
   for (int k = 0; k < R; ++k) {
@@ -164,11 +179,11 @@ __device__ __forceinline__ void process_tile(WaveState<D, G>& S, const KvTile<D>
     const uint32_t pb = bf16_rne(fast_exp2(sc[k] - mref)) << 16;
     S.l[k] += __uint_as_float(pb);
     const uint32_t nb = __float_as_uint(dpp<kDppQuadXor1>(__uint_as_float(pb)));
-    pk[k] = __uint_as_float(__builtin_amdgcn_perm(nb, pb, 0x07060302u));  // lo: own, hi: c+1
+    pk[k] = __uint_as_float(__builtin_amdgcn_perm(nb, pb, pack_sel));
   }
 
   // PV: step h covers tokens 4(2h)+J and 4(2h+1)+J; row r's packed pair is at
-  // position 4(r%4) + 2h of slot r/4 in the same row group.
+  // position pair_pos<r % 4, h> of slot r/4 in the same row group.
   static_for<0, 2>([&](auto hc) {
     constexpr int h = decltype(hc)::value;
     uint32_t vp[DPL];  // (token 2h, token 2h+1) bf16 pairs, one per dim
@@ -182,7 +197,7 @@ __device__ __forceinline__ void process_tile(WaveState<D, G>& S, const KvTile<D>
     }
     static_for<0, G>([&](auto rc) {
       constexpr int r = decltype(rc)::value;
-      const uint32_t pp = __float_as_uint(row_bcast<4 * (r % 4) + 2 * h>(pk[r / 4]));
+      const uint32_t pp = __float_as_uint(row_bcast<pair_pos<r % 4, h>()>(pk[r / 4]));
 #pragma unroll
       for (int d = 0; d < DPL; ++d) S.acc[r][d] = dot2_bf16(pp, vp[d], S.acc[r][d]);
     });
@@ -218,17 +233,19 @@ __device__ __forceinline__ void decode_valu_body(const DecodeParams& p, int wg_i
   // length arrives (j0 < bt_stride for every launched partition).
   const int raw_first = lane < min(64, p.bt_stride - j0) ? bt[lane] : 0;
 
-  // Query slices: lane (J, c) keeps dims (D/16)*c .. of every query row.
+  // Query slices: lane (J, c) keeps dims (D/16)*c .. of every query row, row
+  // r in slot r ^ c/4 (mod 4), the order the reduce-scatter needs.
   uint32_t qv[G][D / 32];
   {
     const uint16_t* qb = p.q + ((size_t)b * p.num_q_heads + h0) * D + (D / 16) * tok;
 #pragma unroll
     for (int r = 0; r < G; ++r) {
+      const int qr = (r & ~3) | ((r & 3) ^ (tok >> 2));
       if constexpr (D == 128) {
-        const uint4 v = *reinterpret_cast<const uint4*>(qb + r * D);
+        const uint4 v = *reinterpret_cast<const uint4*>(qb + qr * D);
         qv[r][0] = v.x; qv[r][1] = v.y; qv[r][2] = v.z; qv[r][3] = v.w;
       } else {
-        const uint2 v = *reinterpret_cast<const uint2*>(qb + r * D);
+        const uint2 v = *reinterpret_cast<const uint2*>(qb + qr * D);
         qv[r][0] = v.x; qv[r][1] = v.y;
       }
     }
@@ -254,7 +271,14 @@ __device__ __forceinline__ void decode_valu_body(const DecodeParams& p, int wg_i
   const uint16_t* kbase = p.k_pool + (size_t)g * kTileElems;
   const uint16_t* vbase = p.v_pool + (size_t)g * kTileElems;
   const size_t item = ((size_t)part * p.batch + b) * p.num_kv_heads + g;
-  const uint32_t lane_off = (uint32_t)(grp * D + (D / 16) * tok) * 2u;
+  // Byte offsets of the lane's slice in row quad u: V in quad order, K in
+  // the order the reduce-scatter needs.
+  uint32_t voff[4], koff[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    voff[u] = (uint32_t)((4 * u + grp) * D + (D / 16) * tok) * 2u;
+    koff[u] = (uint32_t)((4 * (u ^ token_quad(tok)) + grp) * D + (D / 16) * tok) * 2u;
+  }
 
   for (int c0 = 0; c0 < nblk; c0 += 64) {
     const int cn = min(64, nblk - c0);
@@ -266,8 +290,8 @@ __device__ __forceinline__ void decode_valu_body(const DecodeParams& p, int wg_i
       const bool ok = i < cn;
       const size_t id = (size_t)__builtin_amdgcn_readlane(idc, ok ? i : 0);
       const int bytes = ok ? 16 * D * 2 : 0;
-      load_rows<D>(T.k, kbase + id * blk_stride, lane_off, bytes);
-      load_rows<D>(T.v, vbase + id * blk_stride, lane_off, bytes);
+      load_rows<D>(T.k, kbase + id * blk_stride, koff, bytes);
+      load_rows<D>(T.v, vbase + id * blk_stride, voff, bytes);
     };
     auto run = [&](const KvTile<D>& T, int i) {
       const int valid = min(16, end - (start + (c0 + i) * 16));
