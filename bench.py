@@ -263,7 +263,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE={world}); "
-              "the hot path is not distributed in this build", file=sys.stderr)
+              "the decode-attention path runs on a single GPU", file=sys.stderr)
         sys.exit(2)
 
     from workloads import build_config

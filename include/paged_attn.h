@@ -79,8 +79,8 @@ int32_t pa_version(void);
 /* ---------------------------------------------------------------------------
  * KV block pool: layout plus a host-side allocator with reference counts.
  *
- * One pool per stage engine (paper section 2: "a dedicated engine pool for
- * every workflow stage", each with "its own queue, cache").  A block that
+ * One pool per stage engine: the paper gives every stage of the workflow its
+ * own engine pool, with a queue and a cache of its own (section 2).  A block that
  * holds shared prompt tokens is retained once per extra sequence that maps
  * it and returns to the free list when its count reaches zero.
  * ------------------------------------------------------------------------- */

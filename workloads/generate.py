@@ -7,8 +7,8 @@ path both consume what it returns and neither is imported here.
 
 The stage shapes mirror the NL2SQL agent of the paper (section 1 and section 2,
 Fig. 1): an SQL-generator stage whose calls all share one resident schema
-prompt, an SQL-error-fixer stage whose retries share the schema prompt and the
-first attempt ("five refinement attempts against the same schema"), a single
+prompt, an SQL-error-fixer stage whose retries (up to five per request) share
+the schema prompt and the first attempt, a single
 shared engine pool that mixes both stages without stage isolation (Fig. 2's
 contrast case), and a long-context stage pool.
 
