@@ -250,6 +250,36 @@ int paged_attn_decode_trace(const pa_kv_pool *pool, const void *q, const int32_t
                             void *stream);
 
 /* ---------------------------------------------------------------------------
+ * KV append.
+ *
+ * Every decode step adds the key and value rows of the token it produced to
+ * the sequence's resident context before the step's attention reads it (the
+ * paper keeps a stage's context in its engines' cache across calls: section
+ * 2, "Cortex Benefits"; section 3, "Agentic State").
+ * ------------------------------------------------------------------------- */
+
+/* Write the new token's K and V rows: for every sequence b with
+ * n = context_lens[b] >= 1 and every KV head g,
+ *     K pool[block_tables[b][(n-1) / 16]][g][(n-1) % 16][:] = k_new[b][g][:]
+ * and likewise for V.  Sequences with n = 0 append nothing; nothing else in
+ * the pools changes.
+ *   pool          geometry and the K/V device pools (written)
+ *   k_new, v_new  device bf16 [batch][num_kv_heads][head_dim], 16-byte aligned
+ *   block_tables  device int32 [batch][bt_stride]; entry (n-1)/16 of row b
+ *                 must be a block that belongs to sequence b alone: allocate
+ *                 one (kv_pool_alloc) whenever n-1 is a multiple of 16, and
+ *                 copy a shared block before writing into it
+ *   context_lens  device int32 [batch]: lengths including the new token
+ *   batch         >= 0 (0 is a no-op)
+ * Device data is clamped like the decode's: lengths into [0, 16*bt_stride],
+ * ids into [0, num_blocks), so bad data writes a wrong slot inside the pool,
+ * never outside it.  Run the step's decode after this call on the same
+ * stream. */
+int paged_attn_append_kv(const pa_kv_pool *pool, const void *k_new, const void *v_new,
+                         const int32_t *block_tables, int32_t bt_stride,
+                         const int32_t *context_lens, int32_t batch, void *stream);
+
+/* ---------------------------------------------------------------------------
  * Measurement helper.
  * ------------------------------------------------------------------------- */
 

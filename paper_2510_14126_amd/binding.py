@@ -46,6 +46,7 @@ SIGNATURES = {
     "paged_attn_decode_trace": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32,
                                          _i32, _vp, _vp, _vp, _vp, _i64, _vp]),
     "pa_stream_copy": (_c_int, [_vp, _vp, _sz, _vp]),
+    "paged_attn_append_kv": (_c_int, [_vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp]),
     "paged_attn_cascade_workspace_size": (_c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _i32,
                                                    ctypes.POINTER(_sz), ctypes.POINTER(_sz),
                                                    _pi32]),
@@ -240,6 +241,12 @@ def paged_attn_decode_trace(pool: KVPool, q, block_tables, bt_stride, context_le
 
 def pa_stream_copy(src, dst, nbytes, stream=None) -> None:
     _check(_lib.pa_stream_copy(_ptr(src), _ptr(dst), nbytes, _ptr(stream)))
+
+
+def paged_attn_append_kv(pool: KVPool, k_new, v_new, block_tables, bt_stride, context_lens, batch,
+                         stream=None) -> None:
+    _check(_lib.paged_attn_append_kv(pool._handle(), _ptr(k_new), _ptr(v_new), _ptr(block_tables),
+                                     bt_stride, _ptr(context_lens), batch, _ptr(stream)))
 
 
 def paged_attn_cascade_workspace_size(batch, num_q_heads, head_dim, max_context_len,

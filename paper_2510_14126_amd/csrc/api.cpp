@@ -15,8 +15,8 @@ struct pa_kv_pool {
   int32_t num_blocks;
   int32_t num_kv_heads;
   int32_t head_dim;
-  const uint16_t* k;
-  const uint16_t* v;
+  uint16_t* k;                     // caller-owned device pools (the append writes them)
+  uint16_t* v;
   std::vector<int32_t> refcount;  // 0 = free
   std::vector<int32_t> free_stack; // top = back(); ids pop in ascending order initially
 };
@@ -257,8 +257,8 @@ int kv_pool_create(int32_t num_blocks, int32_t block_size, int32_t num_kv_heads,
   p->num_blocks = num_blocks;
   p->num_kv_heads = num_kv_heads;
   p->head_dim = head_dim;
-  p->k = static_cast<const uint16_t*>(k_pool);
-  p->v = static_cast<const uint16_t*>(v_pool);
+  p->k = static_cast<uint16_t*>(k_pool);
+  p->v = static_cast<uint16_t*>(v_pool);
   p->refcount.assign(num_blocks, 0);
   rebuild_free(p);
   *out = p;
@@ -561,6 +561,39 @@ int paged_attn_reduce_cascade(const float* partial_out, const float* partial_lse
   const int32_t pre_parts = (prefix_len + prefix_partition_size - 1) / prefix_partition_size;
   return reduce_impl(partial_out, partial_lse, context_lens, batch, num_q_heads, head_dim,
                      partition_size, max_partitions, pre_parts, prefix_len, out, stream, fn);
+}
+
+int paged_attn_append_kv(const pa_kv_pool* pool, const void* k_new, const void* v_new,
+                         const int32_t* block_tables, int32_t bt_stride, const int32_t* context_lens,
+                         int32_t batch, void* stream) {
+  const char* fn = "paged_attn_append_kv";
+  if (!pool) return fail(PA_EINVAL, "%s: pool is NULL", fn);
+  if (batch < 0) return fail(PA_EINVAL, "%s: batch = %d < 0", fn, batch);
+  if (bt_stride < 1) return fail(PA_EINVAL, "%s: bt_stride = %d < 1", fn, bt_stride);
+  if ((int64_t)bt_stride * PA_BLOCK_SIZE > 0x7fffffffLL)
+    return fail(PA_EINVAL, "%s: bt_stride = %d too large", fn, bt_stride);
+  if (batch == 0) return PA_OK;
+  if (!k_new || !v_new || !block_tables || !context_lens)
+    return fail(PA_EINVAL, "%s: k_new, v_new, block_tables and context_lens must be non-NULL", fn);
+  if (!aligned(k_new, 16) || !aligned(v_new, 16))
+    return fail(PA_EINVAL, "%s: k_new/v_new are not 16-byte aligned", fn);
+  if (!aligned(block_tables, 4) || !aligned(context_lens, 4))
+    return fail(PA_EINVAL, "%s: block_tables/context_lens are not 4-byte aligned", fn);
+  pa::AppendParams p{};
+  p.k_pool = pool->k;
+  p.v_pool = pool->v;
+  p.k_new = static_cast<const uint16_t*>(k_new);
+  p.v_new = static_cast<const uint16_t*>(v_new);
+  p.block_tables = block_tables;
+  p.context_lens = context_lens;
+  p.num_blocks = pool->num_blocks;
+  p.num_kv_heads = pool->num_kv_heads;
+  p.head_dim = pool->head_dim;
+  p.bt_stride = bt_stride;
+  p.batch = batch;
+  hipError_t e = pa::launch_append(p, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
+  return PA_OK;
 }
 
 int pa_stream_copy(const void* src, void* dst, size_t bytes, void* stream) {

@@ -99,6 +99,21 @@ hipError_t launch_cascade(const PrefixParams& pp, const DecodeParams& dp, int gr
                           hipStream_t stream);
 // Log-sum-exp merge of split-KV partials into the bf16 output.
 hipError_t launch_reduce(const ReduceParams& p, int head_dim, hipStream_t stream);
+// Append of one token's K and V rows per sequence.
+struct AppendParams {
+  uint16_t* k_pool;              // bf16 [num_blocks][num_kv_heads][16][head_dim]
+  uint16_t* v_pool;
+  const uint16_t* k_new;         // bf16 [batch][num_kv_heads][head_dim]
+  const uint16_t* v_new;
+  const int32_t* block_tables;   // [batch][bt_stride]
+  const int32_t* context_lens;   // [batch], the new token included
+  int32_t num_blocks;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t bt_stride;
+  int32_t batch;
+};
+hipError_t launch_append(const AppendParams& p, hipStream_t stream);
 // Streaming device copy (measurement helper).
 hipError_t launch_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
 

@@ -24,7 +24,7 @@ def declared_functions():
 
 def test_header_and_library_agree():
     names = declared_functions()
-    assert len(names) == 20, names
+    assert len(names) == 21, names
     lib = pa.library()
     for n in names:
         assert hasattr(lib, n), f"library does not export {n}"
@@ -189,3 +189,37 @@ def test_trace_capacity_checked():
 def test_stream_copy_validation():
     with pytest.raises(pa.PagedAttnError):
         pa.pa_stream_copy(0x1000, 0x2000, 17)
+
+
+# --------------------------------------------------------------- KV append
+
+def _append(pool, **over):
+    a = dict(k_new=0x30000, v_new=0x40000, block_tables=0x50000, bt_stride=4, context_lens=0x60000,
+             batch=2)
+    a.update(over)
+    pa.paged_attn_append_kv(pool, a["k_new"], a["v_new"], a["block_tables"], a["bt_stride"],
+                            a["context_lens"], a["batch"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(batch=-1), pa.PA_EINVAL),
+    (dict(bt_stride=0), pa.PA_EINVAL),
+    (dict(bt_stride=1 << 28), pa.PA_EINVAL),
+    (dict(k_new=0), pa.PA_EINVAL),
+    (dict(v_new=0), pa.PA_EINVAL),
+    (dict(block_tables=0), pa.PA_EINVAL),
+    (dict(context_lens=0), pa.PA_EINVAL),
+    (dict(k_new=0x30008), pa.PA_EINVAL),       # not 16-byte aligned
+    (dict(context_lens=0x60002), pa.PA_EINVAL),
+])
+def test_append_validation(over, code):
+    p = make_pool()
+    with pytest.raises(pa.PagedAttnError) as e:
+        _append(p, **over)
+    assert e.value.code == code, pa.pa_last_error()
+    assert "paged_attn_append_kv" in pa.pa_last_error()
+
+
+def test_append_empty_batch_is_a_no_op():
+    p = make_pool()
+    _append(p, batch=0, k_new=0, v_new=0, block_tables=0, context_lens=0)
