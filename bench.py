@@ -409,6 +409,39 @@ def main():
     torch.cuda.synchronize()
     hot_ms = float(np.mean([a.elapsed_time(b) for a, b in hot])) if hot else None
 
+    # KV append of the step's new token, timed the same way.  The rows written
+    # are the ones already stored at slot ctx-1, so the pools stay unchanged
+    # for the parity check below.
+    nz = w.context_lens > 0
+    last = np.maximum(w.context_lens.astype(np.int64) - 1, 0)
+    phys = w.block_tables[np.arange(w.batch), last // 16]
+    k_new = torch.from_numpy(np.ascontiguousarray(w.k_pool[phys, :, last % 16, :]).view(np.int16)).to(dev)
+    v_new = torch.from_numpy(np.ascontiguousarray(w.v_pool[phys, :, last % 16, :]).view(np.int16)).to(dev)
+    e_app = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for i in range(3):
+        binding.paged_attn_append_kv(reps[i % R][0], k_new, v_new, base.bt, base.bt_stride, base.ctx,
+                                     base.batch, sh)
+    torch.cuda.synchronize()
+    e_app[0].record(stream)
+    for i in range(K):
+        binding.paged_attn_append_kv(reps[i % R][0], k_new, v_new, base.bt, base.bt_stride, base.ctx,
+                                     base.batch, sh)
+    e_app[1].record(stream)
+    torch.cuda.synchronize()
+    app_ms = e_app[0].elapsed_time(e_app[1]) / K
+    app_bytes = 4 * int(nz.sum()) * w.num_kv_heads * w.head_dim * 2      # K+V rows read and written
+    append_line = {"us_per_call": round(app_ms * 1e3, 3), "bytes_per_call": app_bytes,
+                   "gbps": round(app_bytes / (app_ms * 1e-3) / 1e9, 2),
+                   "note": "one launch per step; launch-latency bound at these sizes"}
+    if cpu is not None:
+        from oracle import append_kv
+        kn_h, vn_h = w.k_pool[phys, :, last % 16, :], w.v_pool[phys, :, last % 16, :]
+        c0 = time.perf_counter()
+        append_kv(w.k_pool, w.v_pool, w.block_tables, w.context_lens, kn_h, vn_h)
+        cpu_s = time.perf_counter() - c0
+        append_line["cpu_oracle_us_per_call"] = round(cpu_s * 1e6, 1)
+        append_line["cpu_oracle_note"] = "numpy oracle, one call on one core (it copies both pools)"
+
     # achievable copy bandwidth on this machine (read + write bytes)
     src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
@@ -481,6 +514,7 @@ def main():
                      "kernel": kernel_display_name(w, kern),
                      "launch": "decode call (all kernels it launches)",
                      "bytes_per_launch": int(alg_bytes)},
+        "append_kv": append_line,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
