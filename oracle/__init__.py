@@ -5,7 +5,8 @@ may import this package.  It shares no code with the HIP path.
 
 Modules: ``attention`` (fp64 numpy oracle, split partials and their merge),
 ``brute`` (pure-Python fsum brute force), ``gate`` (parity tolerance),
-``kvcache`` (appending a decode step's K/V to the paged cache).
+``kvcache`` (appending a decode step's K/V to the paged cache), ``extend``
+(causal attention of a chunk of new tokens over the paged cache).
 Every function is pinned by the CPU tests against closed forms, invariants,
 brute force and hand-derived golden values; no function is parity-unpinned.
 """
@@ -14,4 +15,5 @@ from .attention import (  # noqa: F401
     softmax_attention, split_partials,
 )
 from .gate import GateReport, compare  # noqa: F401
+from .extend import extend_attention  # noqa: F401
 from .kvcache import append_kv  # noqa: F401
