@@ -280,6 +280,44 @@ int paged_attn_append_kv(const pa_kv_pool *pool, const void *k_new, const void *
                          const int32_t *context_lens, int32_t batch, void *stream);
 
 /* ---------------------------------------------------------------------------
+ * Extend (chunked prefill) attention.
+ *
+ * A retry of the SQL error fixer sends new prompt tokens that attend to the
+ * stage's resident context (the shared schema prompt and the first attempt)
+ * and, causally, to each other (Cortex paper, section 1, motivating example;
+ * section 2, "Cortex Benefits").  With the chunk's K/V already appended to
+ * the paged cache, token i of sequence b's chunk sits at position
+ * p = n_b - L_b + i and attends to tokens 0 .. p:
+ *
+ *     out[q_start[b] + i][h] = sum_{t <= p} softmax_t(scale * <q[q_start[b] + i][h], K_g[t]>) V_g[t]
+ * ------------------------------------------------------------------------- */
+
+/* Causal attention of each sequence's chunk of new tokens over its paged
+ * context, on matrix-core tiles.
+ *   pool             geometry and K/V device pools; head_dim must be 128
+ *   q                device bf16 [total_q][num_q_heads][128], 16-byte
+ *                    aligned; chunk b is rows q_start[b] .. q_start[b+1]-1
+ *   q_start          device int32 [batch + 1], nondecreasing, q_start[0] = 0,
+ *                    q_start[batch] = total_q
+ *   total_q          rows of q and out
+ *   block_tables     as in paged_attn_decode, covering each context_lens[b]
+ *   context_lens     device int32 [batch]: n_b, the chunk included
+ *                    (L_b = q_start[b+1] - q_start[b] <= n_b)
+ *   num_q_heads      G = num_q_heads / num_kv_heads must be 4 or 8
+ *   max_context_len  host bound of context_lens, at most 8192
+ *                    (PA_EUNSUPPORTED above); sizes the stream
+ *   max_chunk        host bound of the chunk lengths; sizes the grid
+ *   out              device bf16 [total_q][num_q_heads][128], 16-byte aligned
+ * Device data is clamped into the buffers' bounds (chunk lengths into
+ * [0, min(n_b, max_chunk)] and rows into [0, total_q)), so bad data gives
+ * unspecified values, never an out-of-bounds access. */
+int paged_attn_extend(const pa_kv_pool *pool, const void *q, const int32_t *q_start,
+                      int32_t total_q, const int32_t *block_tables, int32_t bt_stride,
+                      const int32_t *context_lens, int32_t batch, int32_t num_q_heads,
+                      float scale, int32_t max_context_len, int32_t max_chunk, void *out,
+                      void *stream);
+
+/* ---------------------------------------------------------------------------
  * Measurement helper.
  * ------------------------------------------------------------------------- */
 

@@ -47,6 +47,8 @@ SIGNATURES = {
                                          _i32, _vp, _vp, _vp, _vp, _i64, _vp]),
     "pa_stream_copy": (_c_int, [_vp, _vp, _sz, _vp]),
     "paged_attn_append_kv": (_c_int, [_vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp]),
+    "paged_attn_extend": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _i32, _i32, _f32, _i32, _i32,
+                                   _vp, _vp]),
     "paged_attn_cascade_workspace_size": (_c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _i32,
                                                    ctypes.POINTER(_sz), ctypes.POINTER(_sz),
                                                    _pi32]),
@@ -277,3 +279,10 @@ def paged_attn_reduce_cascade(partial_out, partial_lse, context_lens, batch, num
                                           _ptr(context_lens), batch, num_q_heads, head_dim,
                                           partition_size, prefix_len, prefix_partition_size,
                                           max_partitions, _ptr(out), _ptr(stream)))
+
+
+def paged_attn_extend(pool: KVPool, q, q_start, total_q, block_tables, bt_stride, context_lens, batch,
+                      num_q_heads, scale, max_context_len, max_chunk, out, stream=None) -> None:
+    _check(_lib.paged_attn_extend(pool._handle(), _ptr(q), _ptr(q_start), total_q, _ptr(block_tables),
+                                  bt_stride, _ptr(context_lens), batch, num_q_heads, scale,
+                                  max_context_len, max_chunk, _ptr(out), _ptr(stream)))

@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB_PATH = os.path.join(HERE, "libpaged_attn.so")
-SOURCES = ["api.cpp", "decode_valu.hip", "decode_mfma.hip", "cascade.hip", "reduce.hip", "append.hip",
+SOURCES = ["api.cpp", "decode_valu.hip", "decode_mfma.hip", "cascade.hip", "reduce.hip", "append.hip", "extend.hip",
            "stream_copy.hip"]
 ARCH = "gfx950"
 

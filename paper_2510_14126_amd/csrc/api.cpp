@@ -563,6 +563,54 @@ int paged_attn_reduce_cascade(const float* partial_out, const float* partial_lse
                      partition_size, max_partitions, pre_parts, prefix_len, out, stream, fn);
 }
 
+int paged_attn_extend(const pa_kv_pool* pool, const void* q, const int32_t* q_start, int32_t total_q,
+                      const int32_t* block_tables, int32_t bt_stride, const int32_t* context_lens,
+                      int32_t batch, int32_t num_q_heads, float scale, int32_t max_context_len,
+                      int32_t max_chunk, void* out, void* stream) {
+  const char* fn = "paged_attn_extend";
+  DecodeArgs a{pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale, max_context_len};
+  int32_t group = 0;
+  int rc = validate_decode(a, &group, fn);
+  if (rc) return rc;
+  if (pool->head_dim != 128)
+    return fail(PA_EUNSUPPORTED, "%s: head_dim = %d (the extend tiles need 128)", fn, pool->head_dim);
+  if (max_context_len > pa::kExtendMaxTokens)
+    return fail(PA_EUNSUPPORTED, "%s: max_context_len = %d exceeds %d", fn, max_context_len,
+                pa::kExtendMaxTokens);
+  if (total_q < 0) return fail(PA_EINVAL, "%s: total_q = %d < 0", fn, total_q);
+  if (max_chunk < 0 || max_chunk > max_context_len)
+    return fail(PA_EINVAL, "%s: max_chunk = %d outside [0, max_context_len = %d]", fn, max_chunk,
+                max_context_len);
+  const int64_t groups = ((int64_t)max_chunk * group + 63) / 64;
+  if ((int64_t)batch * groups * pool->num_kv_heads > 0x7fffffffLL)
+    return fail(PA_EINVAL, "%s: grid too large", fn);
+  if (batch == 0 || total_q == 0 || max_chunk == 0) return PA_OK;
+  if (!q_start || !out) return fail(PA_EINVAL, "%s: q_start and out must be non-NULL", fn);
+  if (!aligned(q_start, 4)) return fail(PA_EINVAL, "%s: q_start is not 4-byte aligned", fn);
+  if (!aligned(out, 16)) return fail(PA_EINVAL, "%s: out is not 16-byte aligned", fn);
+  pa::ExtendParams p{};
+  p.k_pool = pool->k;
+  p.v_pool = pool->v;
+  p.q = static_cast<const uint16_t*>(q);
+  p.q_start = q_start;
+  p.block_tables = block_tables;
+  p.context_lens = context_lens;
+  p.out = static_cast<uint16_t*>(out);
+  p.num_blocks = pool->num_blocks;
+  p.num_kv_heads = pool->num_kv_heads;
+  p.num_q_heads = num_q_heads;
+  p.batch = batch;
+  p.bt_stride = bt_stride;
+  p.max_ctx = max_context_len;
+  p.max_chunk = max_chunk;
+  p.total_q = total_q;
+  p.groups = (int32_t)groups;
+  p.scale_log2 = scale * 1.4426950408889634f;
+  hipError_t e = pa::launch_extend(p, group, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
+  return PA_OK;
+}
+
 int paged_attn_append_kv(const pa_kv_pool* pool, const void* k_new, const void* v_new,
                          const int32_t* block_tables, int32_t bt_stride, const int32_t* context_lens,
                          int32_t batch, void* stream) {

@@ -99,6 +99,30 @@ hipError_t launch_cascade(const PrefixParams& pp, const DecodeParams& dp, int gr
                           hipStream_t stream);
 // Log-sum-exp merge of split-KV partials into the bf16 output.
 hipError_t launch_reduce(const ReduceParams& p, int head_dim, hipStream_t stream);
+// Causal attention of a chunk of new tokens per sequence over its paged
+// context (extend / chunked prefill).
+struct ExtendParams {
+  const uint16_t* k_pool;        // bf16 [num_blocks][num_kv_heads][16][128]
+  const uint16_t* v_pool;
+  const uint16_t* q;             // bf16 [total_q][num_q_heads][128], chunks packed
+  const int32_t* q_start;        // [batch + 1]: chunk b is rows q_start[b] .. q_start[b+1]-1
+  const int32_t* block_tables;   // [batch][bt_stride]
+  const int32_t* context_lens;   // [batch], the chunk included
+  uint16_t* out;                 // bf16 [total_q][num_q_heads][128]
+  int32_t num_blocks;
+  int32_t num_kv_heads;
+  int32_t num_q_heads;
+  int32_t batch;
+  int32_t bt_stride;
+  int32_t max_ctx;               // bound of context_lens (at most kExtendMaxTokens)
+  int32_t max_chunk;             // bound of the chunk lengths
+  int32_t total_q;               // rows of q and out
+  int32_t groups;                // row groups per sequence in the grid
+  float scale_log2;
+};
+hipError_t launch_extend(const ExtendParams& p, int group, hipStream_t stream);
+constexpr int kExtendMaxTokens = 8192;   // context bound of one extend launch
+
 // Append of one token's K and V rows per sequence.
 struct AppendParams {
   uint16_t* k_pool;              // bf16 [num_blocks][num_kv_heads][16][head_dim]

@@ -531,5 +531,163 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
   }
 }
 
+// Causal attention of a chunk of new tokens over its sequence's paged
+// context (extend / chunked prefill).  For KV head g, the (chunk token i,
+// head j) pairs of sequence b form rows R = i*G + j of dense 16-row tiles;
+// row R sees the tokens 0 .. n - L + i (n: context with the chunk, L: chunk
+// length), which is the per-column limit the MFMA core already applies.
+// One workgroup owns four tiles (64 rows, wavefront w: tile w) and streams
+// the sequence's blocks once through LDS for all of them, exactly as the
+// shared-prefix pass does; the stream stops at the workgroup's last visible
+// token.  Each wavefront normalises its rows and writes them as bf16.
+constexpr int kExtendRowsPerWg = 16 * kWaves;
+constexpr int kExtendIdRegs = kExtendMaxTokens / (16 * 64);   // block ids per lane, 64 per register
+
+template <int G>
+__device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_index, lds_u8_t* smem) {
+  const int lane = threadIdx.x & 63;
+  const int wave = wave_uniform(threadIdx.x >> 6);
+  const int q = lane >> 4;
+  const int n = lane & 15;
+
+  int wg = wg_index;
+  const int g = wg % p.num_kv_heads;
+  wg /= p.num_kv_heads;
+  const int grp = wg % p.groups;
+  const int b = wg / p.groups;
+
+  int ctx = p.context_lens[b];
+  ctx = ctx < 0 ? 0 : (ctx > p.max_ctx ? p.max_ctx : ctx);
+  int qs = p.q_start[b];
+  int L = p.q_start[b + 1] - qs;
+  qs = qs < 0 ? 0 : qs;
+  L = L < 0 ? 0 : (L > ctx ? ctx : (L > p.max_chunk ? p.max_chunk : L));
+  L = qs + L > p.total_q ? (p.total_q > qs ? p.total_q - qs : 0) : L;
+  const int rows = L * G;
+  if (grp * kExtendRowsPerWg >= rows) return;          // whole workgroup: no rows here
+  const int row0 = grp * kExtendRowsPerWg + 16 * wave; // this wavefront's tile
+  const int first = ctx - L;                           // position of chunk token 0
+
+  // Tokens the workgroup needs: up to its last row's position.
+  const int last_row = min(rows, (grp + 1) * kExtendRowsPerWg) - 1;
+  const int vis_max = first + last_row / G + 1;
+  const int nblk = (vis_max + 15) >> 4;
+
+  // Block ids of the stream, 64 per register (lane l: blocks l, l+64, ...).
+  int idc[kExtendIdRegs];
+  const int32_t* bt = p.block_tables + (size_t)b * p.bt_stride;
+#pragma unroll
+  for (int r = 0; r < kExtendIdRegs; ++r) {
+    const int j = 64 * r + lane;
+    const int raw = j < nblk ? bt[j] : 0;
+    idc[r] = min(max(raw, 0), p.num_blocks - 1);
+  }
+  auto block_id = [&](int i) {
+    const int r = i >> 6;
+    int v = idc[0];
+#pragma unroll
+    for (int k = 1; k < kExtendIdRegs; ++k)
+      if (r == k) v = idc[k];
+    return __builtin_amdgcn_readlane(v, i & 63);
+  };
+
+  // Column n is row R = row0 + n: chunk token R / G, query head g*G + R % G.
+  uint4 qb[1][4];
+  int lim_col;       // tokens this column sees
+  int min_lim;       // fewest tokens any live column of the tile sees
+  {
+    const int R = row0 + n;
+    const bool ok = R < rows;
+    const int i = ok ? R / G : 0;
+    const uint16_t* qrow = p.q + ((size_t)(qs + i) * p.num_q_heads + g * G + R % G) * kD;
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      qb[0][s] = ok ? *reinterpret_cast<const uint4*>(qrow + (4 * s + q) * 8) : make_uint4(0, 0, 0, 0);
+    lim_col = ok ? first + i + 1 : 0;
+    const int for_min = ok ? lim_col : 0x3fffffff;
+    min_lim = __builtin_amdgcn_readfirstlane(-(int)group_max4(row_max16(-(float)for_min)));
+  }
+
+  MfmaState<1> S;
+  S.m[0] = -__builtin_inff();
+  S.l[0] = 0.f;
+#pragma unroll
+  for (int blk = 0; blk < 8; ++blk) S.o[0][blk] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+  constexpr size_t kTileElems = 16 * kD;
+  const size_t blk_stride = (size_t)p.num_kv_heads * kTileElems;
+  const int share_off = ((4 * wave + q) * kD + n * 8) * 2;   // token row 4*wave + q, chunk n
+  const uint16_t* kbase = p.k_pool + (size_t)g * kTileElems;
+  const uint16_t* vbase = p.v_pool + (size_t)g * kTileElems;
+  auto load = [&](uint4 (&dst)[2], int i) {
+    const bool ok = i < nblk;
+    const size_t id = (size_t)block_id(ok ? i : 0);
+    const int bytes = ok ? (int)(kTileElems * 2) : 0;
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(kbase + id * blk_stride), 0, bytes, kBufferDescWord3);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(vbase + id * blk_stride), 0, bytes, kBufferDescWord3);
+    const auto k = __builtin_amdgcn_raw_buffer_load_b128(rk, share_off, 0, 0);
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(rv, share_off, 0, 0);
+    dst[0] = make_uint4(k[0], k[1], k[2], k[3]);
+    dst[1] = make_uint4(v[0], v[1], v[2], v[3]);
+  };
+
+  uint4 ring[kPrefixRing][2];
+#pragma unroll
+  for (int s = 0; s < kPrefixRing - 1; ++s) load(ring[s], s);
+  for (int i0 = 0; i0 < nblk; i0 += kPrefixRing) {
+#pragma unroll
+    for (int s = 0; s < kPrefixRing; ++s) {
+      const int i = i0 + s;
+      if (i < nblk) {                          // uniform over the workgroup
+        lds_u8_t* st = smem + (i & 1) * kPrefixStageBytes;
+        *reinterpret_cast<lds_u32x4_t*>(st + (4 * wave + q) * kKPitch + n * 16) =
+            u32x4_t{ring[s][0].x, ring[s][0].y, ring[s][0].z, ring[s][0].w};
+        *reinterpret_cast<lds_u32x4_t*>(st + kPrefixKBytes + share_off) =
+            u32x4_t{ring[s][1].x, ring[s][1].y, ring[s][1].z, ring[s][1].w};
+        load(ring[(s + kPrefixRing - 1) % kPrefixRing], i + kPrefixRing - 1);
+        __syncthreads();
+
+        u32x4_t ka[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          ka[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_arow(n) * kKPitch + (4 * c + q) * 16);
+        uint4 vrow[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const u32x4_t v = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixKBytes + ((4 * u + q) * kD + n * 8) * 2);
+          vrow[u] = make_uint4(v[0], v[1], v[2], v[3]);
+        }
+        const int t0 = i * 16;
+        const int valid = min(16, vis_max - t0);
+        const int lim[1] = {min(valid, max(lim_col - t0, 0))};
+        if (valid == 16 && min_lim - t0 >= 16)
+          tile_core<false, 1>(S, ka, vrow, qb, 16, lim, q, p.scale_log2);
+        else
+          tile_core<true, 1>(S, ka, vrow, qb, valid, lim, q, p.scale_log2);
+      }
+    }
+  }
+
+  // Normalise and write bf16: lane (q, n) holds O[rows 4q+r][dims 8n .. 8n+7].
+  const float lcol = group_sum4(S.l[0]);
+  const float inv = lcol > 0.f ? 1.0f / lcol : 0.f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int R = row0 + 4 * q + r;
+    const float f = column_value(inv, q, r);
+    if (R < rows) {
+      uint16_t* orow = p.out + ((size_t)(qs + R / G) * p.num_q_heads + g * G + R % G) * kD + 8 * n;
+      uint4 packed;
+      packed.x = bf16_rne(S.o[0][0][r] * f) | (bf16_rne(S.o[0][1][r] * f) << 16);
+      packed.y = bf16_rne(S.o[0][2][r] * f) | (bf16_rne(S.o[0][3][r] * f) << 16);
+      packed.z = bf16_rne(S.o[0][4][r] * f) | (bf16_rne(S.o[0][5][r] * f) << 16);
+      packed.w = bf16_rne(S.o[0][6][r] * f) | (bf16_rne(S.o[0][7][r] * f) << 16);
+      *reinterpret_cast<uint4*>(orow) = packed;
+    }
+  }
+}
+
 }  // namespace mfma
 }  // namespace pa

@@ -24,7 +24,7 @@ def declared_functions():
 
 def test_header_and_library_agree():
     names = declared_functions()
-    assert len(names) == 21, names
+    assert len(names) == 22, names
     lib = pa.library()
     for n in names:
         assert hasattr(lib, n), f"library does not export {n}"
@@ -223,3 +223,51 @@ def test_append_validation(over, code):
 def test_append_empty_batch_is_a_no_op():
     p = make_pool()
     _append(p, batch=0, k_new=0, v_new=0, block_tables=0, context_lens=0)
+
+
+# --------------------------------------------------------------- extend
+
+def _extend(pool, **over):
+    a = dict(q=0x30000, q_start=0x70000, total_q=64, block_tables=0x50000, bt_stride=8,
+             context_lens=0x60000, batch=2, num_q_heads=32, scale=0.088, max_context_len=128,
+             max_chunk=64, out=0x80000)
+    a.update(over)
+    pa.paged_attn_extend(pool, a["q"], a["q_start"], a["total_q"], a["block_tables"], a["bt_stride"],
+                         a["context_lens"], a["batch"], a["num_q_heads"], a["scale"],
+                         a["max_context_len"], a["max_chunk"], a["out"])
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(batch=-1), pa.PA_EINVAL),
+    (dict(total_q=-1), pa.PA_EINVAL),
+    (dict(max_chunk=-1), pa.PA_EINVAL),
+    (dict(max_chunk=129), pa.PA_EINVAL),           # longer than the context bound
+    (dict(max_context_len=8208, bt_stride=513), pa.PA_EUNSUPPORTED),
+    (dict(bt_stride=7), pa.PA_EINVAL),
+    (dict(num_q_heads=16), pa.PA_EUNSUPPORTED),     # G = 2
+    (dict(q_start=0), pa.PA_EINVAL),
+    (dict(out=0), pa.PA_EINVAL),
+    (dict(out=0x80008), pa.PA_EINVAL),
+    (dict(q=0x30004), pa.PA_EINVAL),
+    (dict(scale=float("nan")), pa.PA_EINVAL),
+])
+def test_extend_validation(over, code):
+    p = make_pool()
+    with pytest.raises(pa.PagedAttnError) as e:
+        _extend(p, **over)
+    assert e.value.code == code, pa.pa_last_error()
+    assert "paged_attn_extend" in pa.pa_last_error()
+
+
+def test_extend_needs_head_dim_128():
+    p = make_pool(d=64)
+    with pytest.raises(pa.PagedAttnError) as e:
+        _extend(p)
+    assert e.value.code == pa.PA_EUNSUPPORTED
+
+
+def test_extend_empty_is_a_no_op():
+    p = make_pool()
+    _extend(p, batch=0, q=0, q_start=0, block_tables=0, context_lens=0, out=0)
+    _extend(p, total_q=0, q_start=0, out=0)
+    _extend(p, max_chunk=0, q_start=0, out=0)

@@ -1,0 +1,120 @@
+"""GPU parity tests of the extend (chunked prefill) attention against the CPU
+oracle.  Every case prints its name before touching the GPU.
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from oracle import compare, extend_attention, paged_decode  # noqa: E402
+from workloads import f32_to_bf16_bits, logical_case, page_case  # noqa: E402
+
+DEV = "cuda:0"
+
+
+def say(msg):
+    print(f"[gpu case] {msg}", flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a visible GPU")
+    yield
+    torch.cuda.empty_cache()
+
+
+def _dev(a):
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a).to(DEV)
+
+
+def make_extend(seed, ctx, chunk, hq=32, hkv=8, prefix_len=0, poison=False):
+    ctx, chunk = list(map(int, ctx)), list(map(int, chunk))
+    case = logical_case(seed, len(ctx), hq, hkv, 128, ctx, prefix_len=prefix_len)
+    w = page_case(case, seed + 1, share_prefix=prefix_len > 0, poison=poison)
+    rng = np.random.default_rng(seed + 2)
+    q_start = np.concatenate([[0], np.cumsum(chunk)]).astype(np.int32)
+    q = f32_to_bf16_bits(rng.standard_normal((int(q_start[-1]), hq, 128), dtype=np.float32))
+    return w, q, q_start
+
+
+def gpu_extend(w, q, q_start, max_chunk=None):
+    from paper_2510_14126_amd import binding
+    total = int(q_start[-1])
+    max_chunk = int(np.max(np.diff(q_start))) if max_chunk is None else max_chunk
+    k_dev, v_dev = _dev(w.k_pool), _dev(w.v_pool)
+    pool = binding.kv_pool_create(w.num_blocks, 16, w.num_kv_heads, 128, k_dev, v_dev)
+    out = torch.zeros((max(total, 1), w.num_q_heads, 128), dtype=torch.int16, device=DEV)
+    q_dev = _dev(q) if total else out
+    binding.paged_attn_extend(pool, q_dev, _dev(q_start), total, _dev(w.block_tables),
+                              int(w.block_tables.shape[1]), _dev(w.context_lens), w.batch,
+                              w.num_q_heads, w.scale, int(w.context_lens.max()), max_chunk, out)
+    torch.cuda.synchronize()
+    pool.close()
+    return out[:total].cpu().numpy().view(np.uint16)
+
+
+def check(w, q, q_start, what, **kw):
+    out = gpu_extend(w, q, q_start, **kw)
+    ref, _ = extend_attention(q, q_start, w.k_pool, w.v_pool, w.block_tables, w.context_lens, w.scale)
+    rep = compare(out, ref)
+    say(f"{what}: {rep}")
+    assert rep.passed, f"{what}: {rep}"
+    return out
+
+
+@pytest.mark.parametrize("hq", [32, 64], ids=["g4", "g8"])
+def test_extend_fixer_shaped(hq):
+    """Retries of one request: a shared schema prefix, a first attempt, and a
+    chunk of new tokens per retry that attends to both and to itself."""
+    rng = np.random.default_rng(50)
+    B = 12
+    chunk = rng.integers(32, 257, B)
+    ctx = 512 + 64 + chunk
+    say(f"extend fixer-shaped hq={hq}: B={B} chunks={chunk.tolist()}")
+    w, q, q_start = make_extend(51, ctx, chunk, hq=hq, prefix_len=512)
+    check(w, q, q_start, f"fixer-shaped g{hq // 8}")
+
+
+CASES = [
+    ("fresh prefill", [1, 15, 16, 17, 100], [1, 15, 16, 17, 100]),
+    ("one-token chunks", [5, 300, 1000], [1, 1, 1]),
+    ("ragged with an empty chunk", [40, 10, 21, 77], [3, 0, 21, 64]),
+    ("chunk across many tiles", [700], [300]),
+]
+
+
+@pytest.mark.parametrize("hq", [32, 64], ids=["g4", "g8"])
+@pytest.mark.parametrize("name,ctx,chunk", CASES, ids=[c[0] for c in CASES])
+def test_extend_edge_shapes(name, ctx, chunk, hq):
+    say(f"extend {name} hq={hq}: ctx={ctx} chunk={chunk}")
+    w, q, q_start = make_extend(61, ctx, chunk, hq=hq, poison=True)
+    check(w, q, q_start, f"{name} g{hq // 8}")
+
+
+def test_extend_loose_max_chunk_bound():
+    say("extend with max_chunk above every chunk")
+    w, q, q_start = make_extend(71, [90, 33], [40, 33])
+    check(w, q, q_start, "loose bound", max_chunk=90)
+
+
+def test_one_token_extend_matches_gpu_decode():
+    from paper_2510_14126_amd.device import PagedBatch
+    say("extend with one-token chunks vs the decode kernel")
+    w, q, q_start = make_extend(81, [200, 513, 47], [1, 1, 1])
+    ext = gpu_extend(w, q, q_start)
+    w.q = q.copy()
+    pb = PagedBatch(w, DEV, partition_size=0)
+    pb.run()
+    torch.cuda.synchronize()
+    dec = pb.out_bits()
+    pb.close()
+    ref, _ = paged_decode(q, w.k_pool, w.v_pool, w.block_tables, w.context_lens, w.scale)
+    assert compare(ext, ref).passed and compare(dec, ref).passed
+    diff = np.abs(ext.astype(np.int32) - dec.astype(np.int32))
+    say(f"extend vs decode: max bf16 ulp difference {int(diff.max())}")
