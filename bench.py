@@ -204,11 +204,11 @@ def ingest_counters(fetch_csv, write_csv, workload_name, kernel_prefix, command_
     print(out)
 
 
-def ingest_stats(stats_csv, workload_name, command_note):
+def ingest_stats(stats_csv, workload_name, command_note, stem=None):
     """Write the kernel-duration summary from a rocprofv3 --stats kernel_stats.csv."""
     import csv
     rows = list(csv.DictReader(open(stats_csv)))
-    out = os.path.join(PROFILE_DIR, f"kernels_{workload_name}_stats.md")
+    out = os.path.join(PROFILE_DIR, f"{stem or f'kernels_{workload_name}_stats'}.md")
     with open(out, "w") as fh:
         fh.write(f"# Kernel durations on the {workload_name} workload (rocprofv3 --kernel-trace --stats)\n\n"
                  f"Command (run from /tmp with TMPDIR=/tmp):\n\n{command_note}\n\n"
@@ -219,6 +219,80 @@ def ingest_stats(stats_csv, workload_name, command_note):
         fh.write("".join(f"\nkernel_source_sha256_16 ({k}): {kernel_source_hash(k)}"
                          for k in KERNEL_SOURCES) + "\n")
     print(out)
+
+
+# ------------------------------------------------------------------ extend
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def extend_chunks(w) -> np.ndarray:
+    """Chunk per sequence: the tokens after the shared prompt (schema prefix and,
+    for the fixer, the request's first attempt); the whole context without one."""
+    shared = 16 * (int(w.meta.get("prefix_blocks", 0)) + int(w.meta.get("mid_blocks", 0)))
+    return np.maximum(w.context_lens.astype(np.int64) - shared, 1).astype(np.int32)
+
+
+def run_extend(w, base, reps, R, K, stream, sh, binding):
+    """Time paged_attn_extend on the workload's batch and spot-check two sequences."""
+    import torch
+    from workloads import f32_to_bf16_bits
+    if w.head_dim != 128 or w.max_context_len > 8192:
+        return {"skipped": "extend needs head_dim 128 and contexts up to 8192 tokens"}
+    chunk = extend_chunks(w)
+    q_start = np.concatenate([[0], np.cumsum(chunk)]).astype(np.int32)
+    total = int(q_start[-1])
+    rng = np.random.default_rng(4242)
+    q = f32_to_bf16_bits(rng.standard_normal((total, w.num_q_heads, w.head_dim), dtype=np.float32))
+    dev = base.q.device
+    q_dev = torch.from_numpy(q.view(np.int16)).to(dev)
+    qs_dev = torch.from_numpy(q_start).to(dev)
+    out = torch.zeros_like(q_dev)
+    max_chunk = int(chunk.max())
+
+    def call(i):
+        binding.paged_attn_extend(reps[i % R][0], q_dev, qs_dev, total, base.bt, base.bt_stride, base.ctx,
+                                  w.batch, w.num_q_heads, w.scale, base.max_ctx, max_chunk, out, sh)
+    for i in range(3):
+        call(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n_calls = max(5, min(K, 50))
+    e0.record(stream)
+    for i in range(n_calls):
+        call(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / n_calls
+    ctx = w.context_lens.astype(np.int64)
+    flops = 0
+    for b in range(w.batch):
+        L, n = int(chunk[b]), int(ctx[b])
+        vis = np.arange(n - L + 1, n + 1, dtype=np.int64)        # tokens each chunk row sees
+        flops += 4 * w.num_q_heads * w.head_dim * int(vis.sum())
+    from workloads import touched_slots
+    alg_bytes = touched_slots(w) * w.bytes_per_token + 2 * total * w.num_q_heads * w.head_dim * 2
+    # parity spot check on the first and the longest-chunk sequence
+    call(0)
+    torch.cuda.synchronize()
+    from oracle import compare, extend_attention
+    seqs = sorted({0, int(np.argmax(chunk))})
+    rows = np.concatenate([np.arange(q_start[b], q_start[b + 1]) for b in seqs])
+    sub_start = np.concatenate([[0], np.cumsum(chunk[seqs])]).astype(np.int32)
+    ref, _ = extend_attention(q[rows], sub_start, w.k_pool, w.v_pool, w.block_tables[seqs],
+                              w.context_lens[seqs], w.scale)
+    rep = compare(out.cpu().numpy().view(np.uint16)[rows], ref)
+    log(f"extend spot check on sequences {seqs}: {rep}")
+    tflops = flops / (ms * 1e-3) / 1e12
+    return {"workload": f"{w.name} batch, chunk = tokens after the shared prompt "
+                        f"({int(chunk.min())}..{max_chunk}, {total} rows)",
+            "kernel": f"extend_mfma_kernel<{w.group}>", "ms_per_call": round(ms, 5),
+            "flops_per_call": flops, "tflops": round(tflops, 1),
+            "roofline": {"bound": "mfma", "achieved": round(tflops, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4)},
+            "alg_kv_gbps": round(alg_bytes / (ms * 1e-3) / 1e9, 1),
+            "parity_spot_check": {"passed": rep.passed, "max_abs": rep.max_abs,
+                                  "worst_row_rel_l2": rep.worst_row_rel_l2, "sequences": seqs}}
 
 
 # ---------------------------------------------------------------- GPU timing
@@ -243,6 +317,11 @@ def main():
     ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--ingest-stats", metavar="KERNEL_STATS_CSV")
     ap.add_argument("--command-note", default="")
+    ap.add_argument("--extend", action="store_true",
+                    help="also time extend (chunked prefill) attention: each sequence's tokens after "
+                         "its shared prompt as the chunk")
+    ap.add_argument("--profile-name", default=None,
+                    help="file stem for --ingest-stats (default kernels_<workload>_stats)")
     ap.add_argument("--profile-loop", type=int, default=0,
                     help="only run this many decode launches (plus one calibration copy) and exit; "
                          "for hardware-counter runs")
@@ -257,7 +336,7 @@ def main():
             plen = 0 if args.cascade == "off" else 16 * int(wc.meta.get("prefix_blocks", 0))
             ingest_counters(*args.ingest_counters, name, decode_kernel_of(wc, plen), args.command_note)
         if args.ingest_stats:
-            ingest_stats(args.ingest_stats, name, args.command_note)
+            ingest_stats(args.ingest_stats, name, args.command_note, args.profile_name)
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -442,6 +521,8 @@ def main():
         append_line["cpu_oracle_us_per_call"] = round(cpu_s * 1e6, 1)
         append_line["cpu_oracle_note"] = "numpy oracle, one call on one core (it copies both pools)"
 
+    extend_line = run_extend(w, base, reps, R, K, stream, sh, binding) if args.extend else None
+
     # achievable copy bandwidth on this machine (read + write bytes)
     src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
@@ -515,6 +596,7 @@ def main():
                      "launch": "decode call (all kernels it launches)",
                      "bytes_per_launch": int(alg_bytes)},
         "append_kv": append_line,
+        "extend": extend_line,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
