@@ -8,7 +8,7 @@ namespace {
 template <int G>
 __global__ void __launch_bounds__(64 * mfma::kWaves) __attribute__((amdgpu_waves_per_eu(2, 8)))
 extend_mfma_kernel(const ExtendParams p) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[mfma::kPrefixLdsBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t smem[mfma::kExtendLdsBytes];
   mfma::extend_mfma_body<G>(p, blockIdx.x, (lds_u8_t*)smem);
 }
 

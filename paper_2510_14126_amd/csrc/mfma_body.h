@@ -200,6 +200,96 @@ __device__ __forceinline__ void tile_core(MfmaState<NT>& S, const u32x4_t (&ka)[
   }
 }
 
+// Two 16-token blocks at once against one column tile.  Lane (q, n) holds
+// the scores of tokens 4r+q (r = 0..3) of both blocks for column n and V
+// rows 4u+q of both blocks, so with the contraction index k = 8q + e standing
+// for token 4e+q of block 0 (e < 4) and token 4(e-4)+q of block 1 (e >= 4),
+// the eight probabilities are exactly the A operand and the eight V rows the
+// B operand of one v_mfma_f32_16x16x32_bf16 per 8 output dims: PV runs at the
+// full bf16 rate and the softmax bookkeeping happens once per 32 tokens.
+// valid0/valid1 and lim0/lim1 as `valid` and `limit` of tile_core, per block
+// (a block with valid = 0 contributes nothing).
+template <bool TAIL>
+__device__ __forceinline__ void tile_core2(MfmaState<1>& S, const u32x4_t (&ka0)[4],
+                                           const u32x4_t (&ka1)[4], const uint4 (&vrow0)[4],
+                                           const uint4 (&vrow1)[4], const uint4 (&qb)[1][4],
+                                           int valid0, int valid1, int lim0, int lim1, int q,
+                                           float scale_log2) {
+  const floatx4_t z = {0.f, 0.f, 0.f, 0.f};
+  floatx4_t a0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+      __builtin_bit_cast(bf16x8_t, ka0[0]), __builtin_bit_cast(bf16x8_t, qb[0][0]), z, 0, 0, 0);
+  floatx4_t a1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+      __builtin_bit_cast(bf16x8_t, ka1[0]), __builtin_bit_cast(bf16x8_t, qb[0][0]), z, 0, 0, 0);
+#pragma unroll
+  for (int s = 1; s < 4; ++s) {
+    a0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka0[s]),
+                                                 __builtin_bit_cast(bf16x8_t, qb[0][s]), a0, 0, 0, 0);
+    a1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka1[s]),
+                                                 __builtin_bit_cast(bf16x8_t, qb[0][s]), a1, 0, 0, 0);
+  }
+
+  float sc[8];
+  bool raise = false;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int r = e & 3;
+    float x = (e < 4 ? a0[r] : a1[r]) * scale_log2;
+    if (TAIL && 4 * r + q >= (e < 4 ? lim0 : lim1)) x = -__builtin_inff();
+    sc[e] = x;
+    raise |= x > S.m[0] + kLazyRescale;
+  }
+  if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+    float b = sc[0];
+#pragma unroll
+    for (int e = 1; e < 8; ++e) b = fmaxf(b, sc[e]);
+    const float bm = group_max4(b);
+    const float mn = bm > S.m[0] + kLazyRescale ? bm : S.m[0];
+    const float alpha = mn == -__builtin_inff() ? 1.f : fast_exp2(S.m[0] - mn);
+    S.l[0] *= alpha;
+    S.m[0] = mn;
+    float ar[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) ar[r] = column_value(alpha, q, r);
+#pragma unroll
+    for (int blk = 0; blk < 8; ++blk)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) S.o[0][blk][r] *= ar[r];
+  }
+
+  const float mref = S.m[0] == -__builtin_inff() ? 0.f : S.m[0];
+  bf16x8_t pa;
+  float lsum = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const __bf16 pb = (__bf16)fast_exp2(sc[e] - mref);
+    lsum += (float)pb;
+    pa[e] = pb;
+  }
+  S.l[0] += lsum;
+
+  uint32_t vw0[4][4], vw1[4][4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const bool k0 = !(TAIL && 4 * u + q >= valid0);
+    const bool k1 = !(TAIL && 4 * u + q >= valid1);
+    vw0[u][0] = k0 ? vrow0[u].x : 0u; vw0[u][1] = k0 ? vrow0[u].y : 0u;
+    vw0[u][2] = k0 ? vrow0[u].z : 0u; vw0[u][3] = k0 ? vrow0[u].w : 0u;
+    vw1[u][0] = k1 ? vrow1[u].x : 0u; vw1[u][1] = k1 ? vrow1[u].y : 0u;
+    vw1[u][2] = k1 ? vrow1[u].z : 0u; vw1[u][3] = k1 ? vrow1[u].w : 0u;
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+    const int w = j >> 1;
+    const u32x4_t vb = {__builtin_amdgcn_perm(vw0[1][w], vw0[0][w], sel),
+                        __builtin_amdgcn_perm(vw0[3][w], vw0[2][w], sel),
+                        __builtin_amdgcn_perm(vw1[1][w], vw1[0][w], sel),
+                        __builtin_amdgcn_perm(vw1[3][w], vw1[2][w], sel)};
+    S.o[0][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, __builtin_bit_cast(bf16x8_t, vb), S.o[0][j],
+                                                        0, 0, 0);
+  }
+}
+
 // Row of the K tile that lane (q, n) supplies as A row n: token 4(n%4) + n/4.
 __device__ __forceinline__ int k_arow(int n) { return 4 * (n & 3) + (n >> 2); }
 
@@ -537,10 +627,13 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
 // row R sees the tokens 0 .. n - L + i (n: context with the chunk, L: chunk
 // length), which is the per-column limit the MFMA core already applies.
 // One workgroup owns four tiles (64 rows, wavefront w: tile w) and streams
-// the sequence's blocks once through LDS for all of them, exactly as the
-// shared-prefix pass does; the stream stops at the workgroup's last visible
-// token.  Each wavefront normalises its rows and writes them as bf16.
+// the sequence's blocks once through LDS for all of them, as the
+// shared-prefix pass does, two blocks per barrier through tile_core2; the
+// stream stops at the workgroup's last visible token.  Each wavefront
+// normalises its rows and writes them as bf16.
 constexpr int kExtendRowsPerWg = 16 * kWaves;
+constexpr int kExtendRing = 6;                  // blocks whose quarter is in flight per wavefront (even)
+constexpr int kExtendLdsBytes = 4 * kPrefixStageBytes;   // two stages of a block pair
 constexpr int kExtendIdRegs = kExtendMaxTokens / (16 * 64);   // block ids per lane, 64 per register
 
 template <int G>
@@ -633,39 +726,57 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
     dst[1] = make_uint4(v[0], v[1], v[2], v[3]);
   };
 
-  uint4 ring[kPrefixRing][2];
+  // Blocks go in pairs: both quarters of a pair are published to one LDS
+  // stage (double-buffered), one barrier, then the two-block core.  An odd
+  // last block pairs with an empty one (valid = 0: fully masked).
+  constexpr int kRing = kExtendRing;
+  uint4 ring[kRing][2];
 #pragma unroll
-  for (int s = 0; s < kPrefixRing - 1; ++s) load(ring[s], s);
-  for (int i0 = 0; i0 < nblk; i0 += kPrefixRing) {
+  for (int s = 0; s < kRing - 2; ++s) load(ring[s], s);
+  const int npair = (nblk + 1) >> 1;
+  for (int j0 = 0; j0 < npair; j0 += kRing / 2) {
 #pragma unroll
-    for (int s = 0; s < kPrefixRing; ++s) {
-      const int i = i0 + s;
-      if (i < nblk) {                          // uniform over the workgroup
-        lds_u8_t* st = smem + (i & 1) * kPrefixStageBytes;
-        *reinterpret_cast<lds_u32x4_t*>(st + (4 * wave + q) * kKPitch + n * 16) =
-            u32x4_t{ring[s][0].x, ring[s][0].y, ring[s][0].z, ring[s][0].w};
-        *reinterpret_cast<lds_u32x4_t*>(st + kPrefixKBytes + share_off) =
-            u32x4_t{ring[s][1].x, ring[s][1].y, ring[s][1].z, ring[s][1].w};
-        load(ring[(s + kPrefixRing - 1) % kPrefixRing], i + kPrefixRing - 1);
+    for (int h = 0; h < kRing / 2; ++h) {
+      const int j = j0 + h;
+      if (j < npair) {                         // uniform over the workgroup
+        lds_u8_t* st = smem + (j & 1) * 2 * kPrefixStageBytes;
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          lds_u8_t* sb = st + e * kPrefixStageBytes;
+          const int s = 2 * h + e;
+          *reinterpret_cast<lds_u32x4_t*>(sb + (4 * wave + q) * kKPitch + n * 16) =
+              u32x4_t{ring[s][0].x, ring[s][0].y, ring[s][0].z, ring[s][0].w};
+          *reinterpret_cast<lds_u32x4_t*>(sb + kPrefixKBytes + share_off) =
+              u32x4_t{ring[s][1].x, ring[s][1].y, ring[s][1].z, ring[s][1].w};
+        }
+        load(ring[(2 * h + kRing - 2) % kRing], 2 * j + kRing - 2);
+        load(ring[(2 * h + kRing - 1) % kRing], 2 * j + kRing - 1);
         __syncthreads();
 
-        u32x4_t ka[4];
+        u32x4_t ka0[4], ka1[4];
+        uint4 vr0[4], vr1[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-          ka[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_arow(n) * kKPitch + (4 * c + q) * 16);
-        uint4 vrow[4];
+        for (int c = 0; c < 4; ++c) {
+          ka0[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_arow(n) * kKPitch + (4 * c + q) * 16);
+          ka1[c] = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + k_arow(n) * kKPitch + (4 * c + q) * 16);
+        }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const u32x4_t v = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixKBytes + ((4 * u + q) * kD + n * 8) * 2);
-          vrow[u] = make_uint4(v[0], v[1], v[2], v[3]);
+          const int off = kPrefixKBytes + ((4 * u + q) * kD + n * 8) * 2;
+          const u32x4_t v0 = *reinterpret_cast<const lds_u32x4_t*>(st + off);
+          const u32x4_t v1 = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + off);
+          vr0[u] = make_uint4(v0[0], v0[1], v0[2], v0[3]);
+          vr1[u] = make_uint4(v1[0], v1[1], v1[2], v1[3]);
         }
-        const int t0 = i * 16;
-        const int valid = min(16, vis_max - t0);
-        const int lim[1] = {min(valid, max(lim_col - t0, 0))};
-        if (valid == 16 && min_lim - t0 >= 16)
-          tile_core<false, 1>(S, ka, vrow, qb, 16, lim, q, p.scale_log2);
+        const int t0 = 2 * j * 16;
+        const int valid0 = max(0, min(16, vis_max - t0));
+        const int valid1 = max(0, min(16, vis_max - t0 - 16));
+        const int lim0 = min(valid0, max(lim_col - t0, 0));
+        const int lim1 = min(valid1, max(lim_col - t0 - 16, 0));
+        if (valid1 == 16 && min_lim - t0 >= 32)
+          tile_core2<false>(S, ka0, ka1, vr0, vr1, qb, 16, 16, lim0, lim1, q, p.scale_log2);
         else
-          tile_core<true, 1>(S, ka, vrow, qb, valid, lim, q, p.scale_log2);
+          tile_core2<true>(S, ka0, ka1, vr0, vr1, qb, valid0, valid1, lim0, lim1, q, p.scale_log2);
       }
     }
   }
