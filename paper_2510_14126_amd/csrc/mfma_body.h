@@ -475,17 +475,18 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
 // kWaves adjacent tiles (wavefront w: tile w) and one prefix partition, and
 // its wavefronts share every block: each loads one quarter (four token rows
 // of K and of V, 2 KiB) into a double-buffered LDS stage, and after a
-// barrier every wavefront runs its own tile against the whole block.  A block
+// barrier every wavefront runs its own tile against the staged blocks, two
+// blocks per barrier through tile_core2.  A block
 // thus crosses from L2 to the CU once per four tiles, and each wavefront owns
 // whole query rows, so no cross-wavefront merge is needed.  All workgroups of
 // a KV head read the same blocks, so each comes from HBM once and from L2
 // afterwards.  Every row writes its (o, lse) partial for the partition,
 // lse = -inf when it attended to nothing.
 constexpr int kPrefixRowsPerWg = 16 * kWaves;
-constexpr int kPrefixRing = 4;                  // blocks whose quarter is in flight per wavefront
+constexpr int kPrefixRing = 4;                  // blocks whose quarter is in flight per wavefront (even)
 constexpr int kPrefixKBytes = 16 * kKPitch;     // staged K tile (A-operand reads need the pitch)
 constexpr int kPrefixStageBytes = kPrefixKBytes + 16 * kD * 2;  // + V tile, row pitch 256
-constexpr int kPrefixLdsBytes = 2 * kPrefixStageBytes;
+constexpr int kPrefixLdsBytes = 4 * kPrefixStageBytes;   // two stages of a block pair
 
 template <int G>
 __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_index, lds_u8_t* smem) {
@@ -560,41 +561,60 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
     dst[1] = make_uint4(v[0], v[1], v[2], v[3]);
   };
 
-  uint4 ring[kPrefixRing][2];
+  // Blocks go in pairs through tile_core2: both quarters of a pair are
+  // published to one LDS stage (double-buffered), one barrier per pair.  The
+  // two blocks of a pair need not be adjacent; an odd last block pairs with an
+  // empty one (valid = 0: fully masked).
+  constexpr int kRing = kPrefixRing;
+  uint4 ring[kRing][2];
 #pragma unroll
-  for (int s = 0; s < kPrefixRing - 1; ++s) load(ring[s], s);
-  for (int i0 = 0; i0 < nblk; i0 += kPrefixRing) {
+  for (int s = 0; s < kRing - 2; ++s) load(ring[s], s);
+  const int npair = (nblk + 1) >> 1;
+  for (int j0 = 0; j0 < npair; j0 += kRing / 2) {
 #pragma unroll
-    for (int s = 0; s < kPrefixRing; ++s) {
-      const int i = i0 + s;
-      if (i < nblk) {                          // uniform over the workgroup
-        lds_u8_t* st = smem + (i & 1) * kPrefixStageBytes;
-        // Publish this wavefront's quarter of block i, then refill the slot
-        // freed last step with the quarter of block i + kPrefixRing - 1.
-        *reinterpret_cast<lds_u32x4_t*>(st + (4 * wave + q) * kKPitch + n * 16) =
-            u32x4_t{ring[s][0].x, ring[s][0].y, ring[s][0].z, ring[s][0].w};
-        *reinterpret_cast<lds_u32x4_t*>(st + kPrefixKBytes + share_off) =
-            u32x4_t{ring[s][1].x, ring[s][1].y, ring[s][1].z, ring[s][1].w};
-        load(ring[(s + kPrefixRing - 1) % kPrefixRing], i + kPrefixRing - 1);
+    for (int h = 0; h < kRing / 2; ++h) {
+      const int j = j0 + h;
+      if (j < npair) {                         // uniform over the workgroup
+        lds_u8_t* st = smem + (j & 1) * 2 * kPrefixStageBytes;
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          lds_u8_t* sb = st + e * kPrefixStageBytes;
+          const int s = 2 * h + e;
+          *reinterpret_cast<lds_u32x4_t*>(sb + (4 * wave + q) * kKPitch + n * 16) =
+              u32x4_t{ring[s][0].x, ring[s][0].y, ring[s][0].z, ring[s][0].w};
+          *reinterpret_cast<lds_u32x4_t*>(sb + kPrefixKBytes + share_off) =
+              u32x4_t{ring[s][1].x, ring[s][1].y, ring[s][1].z, ring[s][1].w};
+        }
+        load(ring[(2 * h + kRing - 2) % kRing], 2 * j + kRing - 2);
+        load(ring[(2 * h + kRing - 1) % kRing], 2 * j + kRing - 1);
         __syncthreads();
 
-        u32x4_t ka[4];
+        u32x4_t ka0[4], ka1[4];
+        uint4 vr0[4], vr1[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-          ka[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_arow(n) * kKPitch + (4 * c + q) * 16);
-        uint4 vrow[4];
+        for (int c = 0; c < 4; ++c) {
+          ka0[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_arow(n) * kKPitch + (4 * c + q) * 16);
+          ka1[c] = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + k_arow(n) * kKPitch + (4 * c + q) * 16);
+        }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const u32x4_t v = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixKBytes + ((4 * u + q) * kD + n * 8) * 2);
-          vrow[u] = make_uint4(v[0], v[1], v[2], v[3]);
+          const int off = kPrefixKBytes + ((4 * u + q) * kD + n * 8) * 2;
+          const u32x4_t v0 = *reinterpret_cast<const lds_u32x4_t*>(st + off);
+          const u32x4_t v1 = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + off);
+          vr0[u] = make_uint4(v0[0], v0[1], v0[2], v0[3]);
+          vr1[u] = make_uint4(v1[0], v1[1], v1[2], v1[3]);
         }
-        const int t0 = start + block_of(i) * 16;
-        const int valid = min(16, end - t0);
-        const int lim[1] = {min(valid, max(ctx - t0, 0))};
-        if (valid == 16 && min_ctx - t0 >= 16)
-          tile_core<false, 1>(S, ka, vrow, qb, 16, lim, q, p.scale_log2);
+        const bool has1 = 2 * j + 1 < nblk;
+        const int ta = start + block_of(2 * j) * 16;
+        const int tb = has1 ? start + block_of(2 * j + 1) * 16 : end;
+        const int valid0 = min(16, end - ta);
+        const int valid1 = has1 ? min(16, end - tb) : 0;
+        const int lim0 = min(valid0, max(ctx - ta, 0));
+        const int lim1 = min(valid1, max(ctx - tb, 0));
+        if (valid0 == 16 && valid1 == 16 && min_ctx - ta >= 16 && min_ctx - tb >= 16)
+          tile_core2<false>(S, ka0, ka1, vr0, vr1, qb, 16, 16, lim0, lim1, q, p.scale_log2);
         else
-          tile_core<true, 1>(S, ka, vrow, qb, valid, lim, q, p.scale_log2);
+          tile_core2<true>(S, ka0, ka1, vr0, vr1, qb, valid0, valid1, lim0, lim1, q, p.scale_log2);
       }
     }
   }
