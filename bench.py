@@ -295,6 +295,91 @@ def run_extend(w, base, reps, R, K, stream, sh, binding):
                                   "worst_row_rel_l2": rep.worst_row_rel_l2, "sequences": seqs}}
 
 
+# --------------------------------------------------------------- footprint
+
+def _blocks_in_use(w) -> int:
+    """Blocks the pool allocator holds for a batch: claim every referenced
+    block once, retain it once per extra table that maps it."""
+    from paper_2510_14126_amd import binding
+    pool = binding.kv_pool_create(w.num_blocks, 16, w.num_kv_heads, w.head_dim, 0x10000, 0x20000)
+    nb = (w.context_lens.astype(np.int64) + 15) // 16
+    used = np.concatenate([w.block_tables[b, : nb[b]] for b in range(w.batch)])
+    ids, counts = np.unique(used, return_counts=True)
+    binding.kv_pool_claim(pool, ids.tolist())
+    extra = np.repeat(ids, counts - 1)
+    if extra.size:
+        binding.kv_pool_retain(pool, extra.tolist())
+    in_use = w.num_blocks - binding.kv_pool_num_free(pool)
+    pool.close()
+    return int(in_use)
+
+
+def _time_steps(w, prefix_len, pps, steps, warmup):
+    import torch
+    from paper_2510_14126_amd.device import PagedBatch
+    pb = PagedBatch(w, torch.device("cuda:0"), prefix_len=prefix_len, prefix_partition_size=pps)
+    for _ in range(warmup):
+        pb.run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        pb.run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    pb.close()
+    return ms
+
+
+def run_footprint(args):
+    """Analogue of the paper's isolated-vs-shared comparison (Fig. 2) on the
+    synthetic stage batches.  Isolated: each stage pool stores its shared
+    prompt blocks once (referenced from every table) and decodes with the
+    shared-prefix cascade.  Shared engine: every sequence holds private copies
+    of its blocks (the shared-pool reading) and decodes with the plain split-KV
+    kernel.  Block counts come from the pool allocator; throughput is measured."""
+    from workloads import CONFIG_NAMES, build_config, duplicate_shared_blocks
+    per_stage = {}
+    tot = dict(blocks_isolated=0, blocks_private=0, seqs=0, ms_isolated=0.0, ms_private=0.0)
+    for k in (2, 3):
+        w = build_config(k)
+        w.partition_size = DEFAULT_PARTITION.get(k, w.partition_size)
+        wd = duplicate_shared_blocks(w)
+        prefix_len = 16 * int(w.meta.get("prefix_blocks", 0))
+        b_iso, b_priv = _blocks_in_use(w), _blocks_in_use(wd)
+        ms_iso = _time_steps(w, prefix_len, default_prefix_partition(k, prefix_len), args.steps, args.warmup)
+        ms_priv = _time_steps(wd, 0, 256, args.steps, args.warmup)
+        bpb = 2 * w.num_kv_heads * 16 * w.head_dim * 2        # K+V bytes per block and layer
+        per_stage[CONFIG_NAMES[k]] = {
+            "sequences": w.batch, "blocks_isolated": b_iso, "blocks_private": b_priv,
+            "kv_mb_per_layer_isolated": round(b_iso * bpb / 1e6, 1),
+            "kv_mb_per_layer_private": round(b_priv * bpb / 1e6, 1),
+            "us_per_step_isolated": round(ms_iso * 1e3, 2), "us_per_step_private": round(ms_priv * 1e3, 2),
+            "tokens_per_s_isolated": round(w.batch / (ms_iso * 1e-3), 1),
+            "tokens_per_s_private": round(w.batch / (ms_priv * 1e-3), 1)}
+        log(f"footprint {CONFIG_NAMES[k]}: {per_stage[CONFIG_NAMES[k]]}")
+        tot["blocks_isolated"] += b_iso
+        tot["blocks_private"] += b_priv
+        tot["seqs"] += w.batch
+        tot["ms_isolated"] += ms_iso
+        tot["ms_private"] += ms_priv
+    line = {
+        "metric": "KV blocks and decode tokens/s: isolated stage pools with shared prompt blocks vs one "
+                  "engine with private copies (generator + fixer batches, one layer)",
+        "stages": per_stage,
+        "total_blocks_isolated": tot["blocks_isolated"], "total_blocks_private": tot["blocks_private"],
+        "footprint_ratio_private_over_isolated": round(tot["blocks_private"] / tot["blocks_isolated"], 3),
+        "admitted_batch_multiplier": round(tot["blocks_private"] / tot["blocks_isolated"], 3),
+        "tokens_per_s_isolated": round(tot["seqs"] / (tot["ms_isolated"] * 1e-3), 1),
+        "tokens_per_s_private": round(tot["seqs"] / (tot["ms_private"] * 1e-3), 1),
+        "note": "admitted_batch_multiplier: how many times more sequences of the same shapes the "
+                "private-copy footprint would hold under isolation (first order: block counts)",
+        "n_gpus": 1, "steps": args.steps, "data": "synthetic",
+    }
+    print(json.dumps(line), flush=True)
+
+
 # ---------------------------------------------------------------- GPU timing
 
 def main():
@@ -320,6 +405,10 @@ def main():
     ap.add_argument("--extend", action="store_true",
                     help="also time extend (chunked prefill) attention: each sequence's tokens after "
                          "its shared prompt as the chunk")
+    ap.add_argument("--footprint", action="store_true",
+                    help="isolated stage pools (shared prompt blocks) vs one engine holding private "
+                         "copies: KV blocks from the pool allocator and measured decode throughput, "
+                         "generator and fixer batches; prints its own JSON line")
     ap.add_argument("--profile-name", default=None,
                     help="file stem for --ingest-stats (default kernels_<workload>_stats)")
     ap.add_argument("--profile-loop", type=int, default=0,
@@ -337,6 +426,10 @@ def main():
             ingest_counters(*args.ingest_counters, name, decode_kernel_of(wc, plen), args.command_note)
         if args.ingest_stats:
             ingest_stats(args.ingest_stats, name, args.command_note, args.profile_name)
+        return
+
+    if args.footprint:
+        run_footprint(args)
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))

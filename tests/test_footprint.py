@@ -1,0 +1,25 @@
+"""Host-side block accounting of the footprint experiment (CPU only): the
+pool allocator's blocks in use equal the distinct blocks the tables map, with
+shared prompt blocks counted once, and equal the sum of per-sequence block
+counts once every sequence holds private copies."""
+import numpy as np
+
+import bench
+from workloads import build_config, duplicate_shared_blocks, logical_case, page_case
+
+
+def test_stage_batches_count_shared_blocks_once():
+    for k in (2, 3):
+        w = build_config(k, values=False)
+        assert bench._blocks_in_use(w) == w.meta["needed_blocks"]
+
+
+def test_private_copies_count_every_sequence():
+    case = logical_case(5, 6, 8, 2, 64, [40, 70, 33, 64, 100, 48], prefix_len=32)
+    w = page_case(case, 6, share_prefix=True)
+    shared = bench._blocks_in_use(w)
+    wd = duplicate_shared_blocks(w)
+    private = bench._blocks_in_use(wd)
+    per_seq = int(((w.context_lens + 15) // 16).sum())
+    assert private == per_seq
+    assert shared == per_seq - (w.batch - 1) * (32 // 16)
