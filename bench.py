@@ -397,6 +397,8 @@ def main():
                     help="shared-prefix cascade (auto: on when the batch shares a prefix)")
     ap.add_argument("--prefix-partition-size", type=int, default=None,
                     help="tokens per prefix partition (default: per workload, see DEFAULT_PREFIX_PARTITION)")
+    ap.add_argument("--schedule", choices=["on", "off"], default="on",
+                    help="run the decode over a host-built work list (non-empty items, longest first)")
     ap.add_argument("--graph", action="store_true",
                     help="replay each step from a captured HIP graph (one per replica)")
     ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
@@ -464,7 +466,18 @@ def main():
     if args.cascade == "off" or (args.cascade == "auto" and prefix_len == 0):
         prefix_len = 0
     pps = args.prefix_partition_size or default_prefix_partition(args.config, prefix_len)
-    base = PagedBatch(w, dev, prefix_len=prefix_len, prefix_partition_size=pps)
+    base = PagedBatch(w, dev, prefix_len=prefix_len, prefix_partition_size=pps,
+                      schedule=args.schedule == "on")
+    sched_host_us = None
+    if base.items is not None:
+        # host cost of the work list (a serving loop rebuilds it every step
+        # from its host context lengths, like the block tables)
+        ts = []
+        for _ in range(50):
+            t1 = time.perf_counter()
+            binding.paged_attn_schedule(w.context_lens, base.max_ctx, base.partition_size, prefix_len)
+            ts.append(time.perf_counter() - t1)
+        sched_host_us = round(1e6 * float(np.median(ts)), 1)
     reps = [(base.pool, base.q)]
     keep = []
     for _ in range(1, R):
@@ -478,6 +491,19 @@ def main():
 
     def decode_on(i, s):
         pool, q = reps[i % R]
+        if base.items is not None:
+            n = int(base.items.numel())
+            if prefix_len:
+                binding.paged_attn_decode_cascade_scheduled(
+                    pool, q, base.bt, base.bt_stride, base.ctx, base.batch, base.hq, w.scale,
+                    base.max_ctx, base.partition_size, prefix_len, base.prefix_partition_size,
+                    base.items, n, base.part_o, base.part_lse, s)
+            else:
+                binding.paged_attn_decode_scheduled(
+                    pool, q, base.bt, base.bt_stride, base.ctx, base.batch, base.hq, w.scale,
+                    base.max_ctx, base.partition_size, base.items, n, base.out, base.part_o,
+                    base.part_lse, s)
+            return
         if prefix_len:
             binding.paged_attn_decode_cascade(pool, q, base.bt, base.bt_stride, base.ctx, base.batch,
                                               base.hq, w.scale, base.max_ctx, base.partition_size,
@@ -668,6 +694,9 @@ def main():
                    "shared_prefix_cascade": {"prefix_len": prefix_len,
                                              "prefix_partition_size": base.prefix_partition_size}
                    if prefix_len else None,
+                   "work_list": (f"host-built, {int(base.items.numel())} non-empty items longest first"
+                                 if base.items is not None else "full grid"),
+                   "work_list_host_us": sched_host_us,
                    "max_context_len": w.max_context_len, "parallelism": "single GPU"},
         "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "decode_steps_per_s": round(1000.0 / ms_step, 2),

@@ -250,6 +250,59 @@ int paged_attn_decode_trace(const pa_kv_pool *pool, const void *q, const int32_t
                             void *stream);
 
 /* ---------------------------------------------------------------------------
+ * Host-built work lists.
+ *
+ * A serving scheduler knows each sequence's context length on the host.
+ * Given them, the library lists only the work items (partition, sequence)
+ * that hold tokens, longest first, so the decode grid carries no empty
+ * partitions and the longest items do not start last.  The order of work
+ * items does not change any result: the scheduled entry points give the same
+ * bits as the unscheduled ones.
+ * ------------------------------------------------------------------------- */
+
+/* Work list of a decode or cascade step from HOST context lengths.
+ *   context_lens     host int32 [batch] (clamped into [0, max_context_len])
+ *   max_context_len, partition_size  as the decode call that will use the list
+ *                    (0 = one partition)
+ *   prefix_len       0 for paged_attn_decode_scheduled; the cascade's
+ *                    prefix_len for paged_attn_decode_cascade_scheduled (its
+ *                    per-sequence partitions cover the tokens after it)
+ *   items            host int32 [capacity]: item = part * batch + b
+ *   num_items        receives the number of items (also when capacity is too
+ *                    small, which returns PA_EINVAL)
+ * Items with no tokens are left out, except in a single-partition decode
+ * without a prefix, where every sequence's item writes its output row.
+ * Items are ordered by descending token count; ties keep the order of the
+ * unscheduled grid (partition-major, or sequence-major when there are 16 or
+ * more partitions). */
+int paged_attn_schedule(const int32_t *context_lens, int32_t batch, int32_t max_context_len,
+                        int32_t partition_size, int32_t prefix_len, int32_t *items,
+                        int32_t capacity, int32_t *num_items);
+
+/* paged_attn_decode over a work list (device int32 [num_items], made by
+ * paged_attn_schedule from the same context lengths, copied to the device).
+ * The list must hold every item with tokens (and, for a single partition,
+ * every sequence); ids are clamped into the grid.  num_items in
+ * [0, partitions * batch]. */
+int paged_attn_decode_scheduled(const pa_kv_pool *pool, const void *q, const int32_t *block_tables,
+                                int32_t bt_stride, const int32_t *context_lens, int32_t batch,
+                                int32_t num_q_heads, float scale, int32_t max_context_len,
+                                int32_t partition_size, const int32_t *items, int32_t num_items,
+                                void *out, float *partial_out, float *partial_lse, void *stream);
+
+/* paged_attn_decode_cascade with the per-sequence partitions taken from a
+ * work list (paged_attn_schedule with the same prefix_len); the prefix pass
+ * is unchanged.  Follow with paged_attn_reduce_cascade. */
+int paged_attn_decode_cascade_scheduled(const pa_kv_pool *pool, const void *q,
+                                        const int32_t *block_tables, int32_t bt_stride,
+                                        const int32_t *context_lens, int32_t batch,
+                                        int32_t num_q_heads, float scale, int32_t max_context_len,
+                                        int32_t partition_size, int32_t prefix_len,
+                                        int32_t prefix_partition_size, const int32_t *items,
+                                        int32_t num_items, float *partial_out,
+                                        float *partial_lse, void *stream);
+
+/* ---------------------------------------------------------------------------
  * KV append.
  *
  * Every decode step adds the key and value rows of the token it produced to

@@ -47,6 +47,11 @@ SIGNATURES = {
                                          _i32, _vp, _vp, _vp, _vp, _i64, _vp]),
     "pa_stream_copy": (_c_int, [_vp, _vp, _sz, _vp]),
     "paged_attn_append_kv": (_c_int, [_vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp]),
+    "paged_attn_schedule": (_c_int, [_pi32, _i32, _i32, _i32, _i32, _pi32, _i32, _pi32]),
+    "paged_attn_decode_scheduled": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32, _i32,
+                                             _vp, _i32, _vp, _vp, _vp, _vp]),
+    "paged_attn_decode_cascade_scheduled": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32,
+                                                     _i32, _i32, _i32, _vp, _i32, _vp, _vp, _vp]),
     "paged_attn_extend": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _i32, _i32, _f32, _i32, _i32,
                                    _vp, _vp]),
     "paged_attn_cascade_workspace_size": (_c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _i32,
@@ -286,3 +291,37 @@ def paged_attn_extend(pool: KVPool, q, q_start, total_q, block_tables, bt_stride
     _check(_lib.paged_attn_extend(pool._handle(), _ptr(q), _ptr(q_start), total_q, _ptr(block_tables),
                                   bt_stride, _ptr(context_lens), batch, num_q_heads, scale,
                                   max_context_len, max_chunk, _ptr(out), _ptr(stream)))
+
+
+def paged_attn_schedule(context_lens, max_context_len, partition_size, prefix_len=0):
+    """Work list (numpy int32, item = part * batch + b) from host context lengths."""
+    import numpy as np
+    ctx = np.ascontiguousarray(np.asarray(context_lens, dtype=np.int32))
+    batch = int(ctx.size)
+    n = ctypes.c_int32()
+    cap = max(1, batch * max(1, -(-max(max_context_len - prefix_len, 1) // partition_size)
+                             if partition_size else 1))
+    items = np.zeros(cap, dtype=np.int32)
+    _check(_lib.paged_attn_schedule(ctx.ctypes.data_as(_pi32), batch, max_context_len, partition_size,
+                                    prefix_len, items.ctypes.data_as(_pi32), cap, ctypes.byref(n)))
+    return items[: n.value].copy()
+
+
+def paged_attn_decode_scheduled(pool: KVPool, q, block_tables, bt_stride, context_lens, batch,
+                                num_q_heads, scale, max_context_len, partition_size, items, num_items,
+                                out, partial_out=None, partial_lse=None, stream=None) -> None:
+    _check(_lib.paged_attn_decode_scheduled(pool._handle(), _ptr(q), _ptr(block_tables), bt_stride,
+                                            _ptr(context_lens), batch, num_q_heads, scale,
+                                            max_context_len, partition_size, _ptr(items), num_items,
+                                            _ptr(out), _ptr(partial_out), _ptr(partial_lse),
+                                            _ptr(stream)))
+
+
+def paged_attn_decode_cascade_scheduled(pool: KVPool, q, block_tables, bt_stride, context_lens, batch,
+                                        num_q_heads, scale, max_context_len, partition_size,
+                                        prefix_len, prefix_partition_size, items, num_items,
+                                        partial_out, partial_lse, stream=None) -> None:
+    _check(_lib.paged_attn_decode_cascade_scheduled(
+        pool._handle(), _ptr(q), _ptr(block_tables), bt_stride, _ptr(context_lens), batch,
+        num_q_heads, scale, max_context_len, partition_size, prefix_len, prefix_partition_size,
+        _ptr(items), num_items, _ptr(partial_out), _ptr(partial_lse), _ptr(stream)))

@@ -6,6 +6,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <string>
@@ -150,9 +151,19 @@ hipError_t launch_decode(const pa::DecodeParams& p, const pa_kv_pool* pool, int3
                                       static_cast<hipStream_t>(stream));
 }
 
+// Checks of an optional host-built work list (items = part * batch + b).
+int validate_items(const int32_t* items, int32_t num_items, int64_t max_items, const char* fn) {
+  if (num_items < 0 || num_items > max_items)
+    return fail(PA_EINVAL, "%s: num_items = %d outside [0, %lld]", fn, num_items, (long long)max_items);
+  if (num_items > 0 && (!items || !aligned(items, 4)))
+    return fail(PA_EINVAL, "%s: items is NULL or not 4-byte aligned", fn);
+  return PA_OK;
+}
+
 int decode_impl(const DecodeArgs& a, int32_t partition_size, void* out, float* partial_out,
                 float* partial_lse, int32_t* trace, int64_t trace_capacity, bool tracing,
-                void* stream, const char* fn) {
+                void* stream, const char* fn, bool scheduled = false,
+                const int32_t* items = nullptr, int32_t num_items = 0) {
   int32_t group = 0;
   int rc = validate_decode(a, &group, fn);
   if (rc) return rc;
@@ -161,6 +172,10 @@ int decode_impl(const DecodeArgs& a, int32_t partition_size, void* out, float* p
   if (rc) return rc;
   const int64_t grid = (int64_t)pl.num_parts * a.batch * a.pool->num_kv_heads;
   if (grid > 0x7fffffffLL) return fail(PA_EINVAL, "%s: grid of %lld workgroups is too large", fn, (long long)grid);
+  if (scheduled) {
+    rc = validate_items(items, num_items, (int64_t)pl.num_parts * a.batch, fn);
+    if (rc) return rc;
+  }
   if (a.batch == 0) return PA_OK;
   const bool split = pl.num_parts > 1;
   if (!split) {
@@ -193,6 +208,10 @@ int decode_impl(const DecodeArgs& a, int32_t partition_size, void* out, float* p
   p.part_stride = pl.num_parts;
   p.write_partials = split ? 1 : 0;
   p.trace_tiles = trace_tiles;
+  if (scheduled) {
+    p.items = items;
+    p.num_items = num_items;
+  }
   hipError_t e = launch_decode(p, a.pool, group, tracing, stream);
   if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
   return PA_OK;
@@ -426,13 +445,14 @@ int paged_attn_cascade_workspace_size(int32_t batch, int32_t num_q_heads, int32_
   return PA_OK;
 }
 
-int paged_attn_decode_cascade(const pa_kv_pool* pool, const void* q, const int32_t* block_tables,
-                              int32_t bt_stride, const int32_t* context_lens, int32_t batch,
-                              int32_t num_q_heads, float scale, int32_t max_context_len,
-                              int32_t partition_size, int32_t prefix_len,
-                              int32_t prefix_partition_size, float* partial_out,
-                              float* partial_lse, void* stream) {
-  const char* fn = "paged_attn_decode_cascade";
+namespace {
+
+int cascade_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tables,
+                 int32_t bt_stride, const int32_t* context_lens, int32_t batch,
+                 int32_t num_q_heads, float scale, int32_t max_context_len,
+                 int32_t partition_size, int32_t prefix_len, int32_t prefix_partition_size,
+                 float* partial_out, float* partial_lse, void* stream, const char* fn,
+                 bool scheduled, const int32_t* items, int32_t num_items) {
   const DecodeArgs a{pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
                      max_context_len};
   int32_t group = 0;
@@ -450,6 +470,10 @@ int paged_attn_decode_cascade(const pa_kv_pool* pool, const void* q, const int32
   const int64_t g_suf = (int64_t)cp.suf_parts * batch * pool->num_kv_heads;
   if (g_pre + g_suf > 0x7fffffffLL)
     return fail(PA_EINVAL, "%s: grid too large", fn);
+  if (scheduled) {
+    rc = validate_items(items, num_items, (int64_t)cp.suf_parts * batch, fn);
+    if (rc) return rc;
+  }
   if (batch == 0) return PA_OK;
   if (!partial_out || !partial_lse) return fail(PA_EINVAL, "%s: partial buffers are NULL", fn);
   if (!aligned(partial_out, 16) || !aligned(partial_lse, 4))
@@ -484,6 +508,10 @@ int paged_attn_decode_cascade(const pa_kv_pool* pool, const void* q, const int32
   p.part_stride = cp.stride;
   p.write_partials = 1;
   p.trace_tiles = cp.suf_tokens / PA_BLOCK_SIZE;
+  if (scheduled) {
+    p.items = items;
+    p.num_items = num_items;
+  }
   if (pool->head_dim == 128) {
     // prefix pass and per-sequence decode in one grid
     hipError_t e = pa::launch_cascade(pp, p, group, st);
@@ -494,6 +522,106 @@ int paged_attn_decode_cascade(const pa_kv_pool* pool, const void* q, const int32
     hipError_t e = launch_decode(p, pool, group, false, stream);
     if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
   }
+  return PA_OK;
+}
+
+// Lengths of the work items of a decode plan, for the host schedule.
+struct ItemLen {
+  int32_t len;
+  int32_t item;   // part * batch + b
+};
+
+}  // namespace
+
+int paged_attn_decode_cascade(const pa_kv_pool* pool, const void* q, const int32_t* block_tables,
+                              int32_t bt_stride, const int32_t* context_lens, int32_t batch,
+                              int32_t num_q_heads, float scale, int32_t max_context_len,
+                              int32_t partition_size, int32_t prefix_len,
+                              int32_t prefix_partition_size, float* partial_out,
+                              float* partial_lse, void* stream) {
+  return cascade_impl(pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
+                      max_context_len, partition_size, prefix_len, prefix_partition_size,
+                      partial_out, partial_lse, stream, "paged_attn_decode_cascade", false, nullptr, 0);
+}
+
+int paged_attn_decode_cascade_scheduled(const pa_kv_pool* pool, const void* q,
+                                        const int32_t* block_tables, int32_t bt_stride,
+                                        const int32_t* context_lens, int32_t batch,
+                                        int32_t num_q_heads, float scale, int32_t max_context_len,
+                                        int32_t partition_size, int32_t prefix_len,
+                                        int32_t prefix_partition_size, const int32_t* items,
+                                        int32_t num_items, float* partial_out, float* partial_lse,
+                                        void* stream) {
+  return cascade_impl(pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
+                      max_context_len, partition_size, prefix_len, prefix_partition_size,
+                      partial_out, partial_lse, stream, "paged_attn_decode_cascade_scheduled", true,
+                      items, num_items);
+}
+
+int paged_attn_decode_scheduled(const pa_kv_pool* pool, const void* q, const int32_t* block_tables,
+                                int32_t bt_stride, const int32_t* context_lens, int32_t batch,
+                                int32_t num_q_heads, float scale, int32_t max_context_len,
+                                int32_t partition_size, const int32_t* items, int32_t num_items,
+                                void* out, float* partial_out, float* partial_lse, void* stream) {
+  const DecodeArgs a{pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
+                     max_context_len};
+  return decode_impl(a, partition_size, out, partial_out, partial_lse, nullptr, 0, false, stream,
+                     "paged_attn_decode_scheduled", true, items, num_items);
+}
+
+int paged_attn_schedule(const int32_t* context_lens, int32_t batch, int32_t max_context_len,
+                        int32_t partition_size, int32_t prefix_len, int32_t* items,
+                        int32_t capacity, int32_t* num_items) {
+  const char* fn = "paged_attn_schedule";
+  if (!num_items) return fail(PA_EINVAL, "%s: num_items is NULL", fn);
+  if (batch < 0) return fail(PA_EINVAL, "%s: batch = %d < 0", fn, batch);
+  if (max_context_len < 0) return fail(PA_EINVAL, "%s: max_context_len = %d < 0", fn, max_context_len);
+  if (partition_size < 0 || partition_size % PA_BLOCK_SIZE != 0)
+    return fail(PA_EINVAL, "%s: partition_size = %d is not a non-negative multiple of %d", fn,
+                partition_size, PA_BLOCK_SIZE);
+  if (prefix_len < 0 || prefix_len > max_context_len)
+    return fail(PA_EINVAL, "%s: prefix_len = %d outside [0, max_context_len]", fn, prefix_len);
+  if (batch > 0 && !context_lens) return fail(PA_EINVAL, "%s: context_lens is NULL", fn);
+  // The partitioning of the call that will use the list.
+  int64_t size, parts;
+  if (prefix_len == 0) {
+    Plan pl;
+    const int rc = plan(max_context_len, partition_size, &pl, fn);
+    if (rc) return rc;
+    size = pl.part_tokens;
+    parts = pl.num_parts;
+  } else {
+    if (partition_size == 0)
+      return fail(PA_EINVAL, "%s: a cascade needs partition_size > 0", fn);
+    size = partition_size;
+    parts = ((int64_t)max_context_len - prefix_len + size - 1) / size;
+  }
+  if (parts * batch > 0x7fffffffLL) return fail(PA_EINVAL, "%s: too many work items", fn);
+  // A single-partition decode without a prefix writes the output row of every
+  // sequence (zeros for an empty one), so every sequence keeps its item; any
+  // split launch skips empty partitions and the reduce covers them.
+  const bool keep_empty = prefix_len == 0 && parts == 1;
+  std::vector<ItemLen> list;
+  list.reserve((size_t)(parts * batch));
+  const bool seq_major = item_order_for((int32_t)parts) == 1;
+  for (int64_t i = 0; i < parts * batch; ++i) {
+    const int64_t part = seq_major ? i % parts : i / batch;
+    const int32_t b = (int32_t)(seq_major ? i / parts : i % batch);
+    int64_t n = context_lens[b];
+    n = n < 0 ? 0 : (n > max_context_len ? max_context_len : n);
+    const int64_t len = std::min<int64_t>(size, n - prefix_len - part * size);
+    if (len > 0 || keep_empty)
+      list.push_back({(int32_t)std::max<int64_t>(len, 0), (int32_t)(part * batch + b)});
+  }
+  // Longest first; ties in the order of the unscheduled grid (sequence-major
+  // from 16 partitions on, else partition-major), so the list is deterministic.
+  std::stable_sort(list.begin(), list.end(),
+                   [](const ItemLen& x, const ItemLen& y) { return x.len > y.len; });
+  *num_items = (int32_t)list.size();
+  if ((int64_t)list.size() > capacity)
+    return fail(PA_EINVAL, "%s: %d work items exceed capacity %d", fn, (int32_t)list.size(), capacity);
+  if (!list.empty() && !items) return fail(PA_EINVAL, "%s: items is NULL", fn);
+  for (size_t i = 0; i < list.size(); ++i) items[i] = list[i].item;
   return PA_OK;
 }
 

@@ -64,7 +64,7 @@ hipError_t launch_cascade(const PrefixParams& pp, const DecodeParams& dp, int gr
   // fastest index of both).
   if (pp.num_kv_heads != dp.num_kv_heads) return hipErrorInvalidValue;
   const int64_t prefix_runs = (int64_t)pp.prefix_parts * row_groups;
-  const int64_t decode_runs = (int64_t)dp.num_parts * dp.batch;
+  const int64_t decode_runs = decode_items(dp);
   const int64_t grid = (prefix_runs + decode_runs) * dp.num_kv_heads;
   if (grid == 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;

@@ -38,7 +38,8 @@ hipError_t launch_prefix_mfma(const PrefixParams& p, int group, hipStream_t stre
 }
 
 hipError_t launch_decode_mfma(const DecodeParams& p, bool trace, hipStream_t stream) {
-  const int64_t grid = (int64_t)p.num_parts * p.batch * p.num_kv_heads;
+  const int64_t grid = decode_items(p) * p.num_kv_heads;
+  if (grid == 0) return hipSuccess;
   if (trace)
     hipLaunchKernelGGL(decode_mfma_g8_kernel<true>, dim3((unsigned)grid), dim3(64 * kWaves), 0,
                        stream, p);

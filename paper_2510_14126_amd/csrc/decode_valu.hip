@@ -16,7 +16,8 @@ template <int D, int G, bool TRACE>
 hipError_t launch_t(const DecodeParams& p, hipStream_t stream) {
   constexpr int W = PA_VALU_WAVES;
   constexpr int NBUF = PA_VALU_NBUF;
-  const int64_t grid = (int64_t)p.num_parts * p.batch * p.num_kv_heads;
+  const int64_t grid = decode_items(p) * p.num_kv_heads;
+  if (grid == 0) return hipSuccess;
   hipLaunchKernelGGL((decode_valu_kernel<D, G, W, NBUF, TRACE>), dim3((unsigned)grid),
                      dim3(64 * W), 0, stream, p);
   return hipGetLastError();

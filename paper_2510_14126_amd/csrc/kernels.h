@@ -31,18 +31,33 @@ struct DecodeParams {
   int32_t write_partials;        // 1: write (o, lse) partials; 0: write the bf16 output
   int32_t trace_tiles;           // trace slots per work item
   int32_t item_order;            // workgroup -> work item order (decode_item)
+  const int32_t* items;          // optional work list: item = part * batch + b, or NULL
+  int32_t num_items;             // entries of items
   float scale_log2;              // softmax scale * log2(e)
 };
+
+// Work items (partition, sequence) of a decode grid; one workgroup per item
+// and KV head.
+__host__ __device__ inline int64_t decode_items(const DecodeParams& p) {
+  return p.items ? (int64_t)p.num_items : (int64_t)p.num_parts * p.batch;
+}
 
 // Work item (KV head g, sequence b, partition part) of decode workgroup wg.
 // The KV head varies fastest, so consecutive workgroups, which the
 // dispatcher deals to the XCDs round-robin, keep one KV head per XCD.  Then
-// either all sequences' partition 0, then partition 1, ... (item_order 0), or
-// all partitions of sequence 0, then sequence 1, ... (item_order 1).
+// the host's work list when there is one, else either all sequences'
+// partition 0, then partition 1, ... (item_order 0), or all partitions of
+// sequence 0, then sequence 1, ... (item_order 1).
 __device__ __forceinline__ void decode_item(const DecodeParams& p, int wg, int& g, int& b, int& part) {
   g = wg % p.num_kv_heads;
   wg /= p.num_kv_heads;
-  if (p.item_order == 0) {
+  if (p.items) {                 // host-built list (device data: clamped into the grid)
+    int it = p.items[wg];
+    const int last = p.num_parts * p.batch - 1;
+    it = it < 0 ? 0 : (it > last ? last : it);
+    b = it % p.batch;
+    part = it / p.batch;
+  } else if (p.item_order == 0) {
     b = wg % p.batch;
     part = wg / p.batch;
   } else {

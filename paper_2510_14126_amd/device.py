@@ -24,7 +24,7 @@ def _dev(a: np.ndarray, device) -> torch.Tensor:
 class PagedBatch:
     def __init__(self, w, device="cuda:0", partition_size: int | None = None,
                  register_blocks: bool = True, k_pool=None, v_pool=None,
-                 prefix_len: int = 0, prefix_partition_size: int = 256):
+                 prefix_len: int = 0, prefix_partition_size: int = 256, schedule: bool = False):
         self.w = w
         self.device = torch.device(device)
         self.partition_size = w.partition_size if partition_size is None else partition_size
@@ -52,6 +52,14 @@ class PagedBatch:
                                                        self.partition_size)
         self.part_o = torch.empty(ob // 4, dtype=torch.float32, device=self.device) if ob else None
         self.part_lse = torch.empty(lb // 4, dtype=torch.float32, device=self.device) if lb else None
+        self.items = None
+        if schedule:
+            self.set_items(binding.paged_attn_schedule(w.context_lens, self.max_ctx,
+                                                       self.partition_size, prefix_len))
+
+    def set_items(self, items) -> None:
+        """Run the per-sequence partitions from a host work list (see paged_attn_schedule)."""
+        self.items = torch.from_numpy(np.ascontiguousarray(items, dtype=np.int32)).to(self.device)
 
     def register_placement(self) -> None:
         """Claim every block the tables use; retain shared blocks once per extra user."""
@@ -70,6 +78,19 @@ class PagedBatch:
         return int(self.w.block_tables.shape[1])
 
     def decode(self, stream=None, out=None) -> None:
+        if self.items is not None:
+            n = int(self.items.numel())
+            if self.prefix_len:
+                binding.paged_attn_decode_cascade_scheduled(
+                    self.pool, self.q, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,
+                    self.w.scale, self.max_ctx, self.partition_size, self.prefix_len,
+                    self.prefix_partition_size, self.items, n, self.part_o, self.part_lse, stream)
+            else:
+                binding.paged_attn_decode_scheduled(
+                    self.pool, self.q, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,
+                    self.w.scale, self.max_ctx, self.partition_size, self.items, n,
+                    self.out if out is None else out, self.part_o, self.part_lse, stream)
+            return
         if self.prefix_len:
             binding.paged_attn_decode_cascade(
                 self.pool, self.q, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,

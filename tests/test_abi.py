@@ -3,8 +3,11 @@
 No kernel is launched here: every call either manipulates host metadata or
 fails validation before any HIP call, so these run without a GPU.
 """
+import ctypes
 import os
 import re
+
+import numpy as np
 
 import pytest
 
@@ -24,7 +27,7 @@ def declared_functions():
 
 def test_header_and_library_agree():
     names = declared_functions()
-    assert len(names) == 22, names
+    assert len(names) == 25, names
     lib = pa.library()
     for n in names:
         assert hasattr(lib, n), f"library does not export {n}"
@@ -271,3 +274,81 @@ def test_extend_empty_is_a_no_op():
     _extend(p, batch=0, q=0, q_start=0, block_tables=0, context_lens=0, out=0)
     _extend(p, total_q=0, q_start=0, out=0)
     _extend(p, max_chunk=0, q_start=0, out=0)
+
+
+# --------------------------------------------------------------- work lists
+
+def _brute_items(ctx, max_ctx, S, prefix):
+    """Every (partition, sequence) item that holds tokens, by brute force.
+
+    The partitioning is the decode call's own (paged_attn_num_partitions) or,
+    with a prefix, S-token partitions after it."""
+    if prefix == 0:
+        parts = pa.paged_attn_num_partitions(max_ctx, S)
+        size = S if parts > 1 else max_ctx + 16
+    else:
+        parts, size = -(-(max_ctx - prefix) // S), S
+    keep_empty = prefix == 0 and parts == 1
+    B = len(ctx)
+    pairs = [(b, part) for b in range(B) for part in range(parts)] if parts >= 16 else \
+        [(b, part) for part in range(parts) for b in range(B)]
+    lst = []
+    for pos, (b, part) in enumerate(pairs):
+        n = min(max(int(ctx[b]), 0), max_ctx)
+        toks = [t for t in range(prefix + part * size, prefix + (part + 1) * size) if t < n]
+        if toks or keep_empty:
+            lst.append((-len(toks), pos, part * B + b))
+    return [it for _, _, it in sorted(lst)]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_schedule_lists_every_item_longest_first(seed):
+    rng = np.random.default_rng(seed)
+    B = int(rng.integers(1, 40))
+    max_ctx = int(rng.integers(1, 3000))
+    ctx = rng.integers(0, max_ctx + 1, B)
+    ctx[0] = max_ctx
+    for S in (0, 16, 128, 512, 4096):
+        for prefix in (0, 16 * int(rng.integers(0, max_ctx // 16 + 1))):
+            if S == 0 and prefix:
+                with pytest.raises(pa.PagedAttnError):
+                    pa.paged_attn_schedule(ctx, max_ctx, S, prefix)
+                continue
+            got = pa.paged_attn_schedule(ctx, max_ctx, S, prefix)
+            assert list(got) == _brute_items(ctx, max_ctx, S, prefix), (S, prefix)
+
+
+@pytest.mark.parametrize("max_ctx,S", [(0, 64), (0, 0), (20, 32), (32, 32), (33, 32)])
+def test_schedule_matches_the_decode_partitioning(max_ctx, S):
+    """A call whose decode runs one partition keeps every sequence's item,
+    also when no sequence holds a token."""
+    ctx = [0, max_ctx, max_ctx // 2]
+    got = list(pa.paged_attn_schedule(ctx, max_ctx, S))
+    assert got == _brute_items(ctx, max_ctx, S, 0)
+    if pa.paged_attn_num_partitions(max_ctx, S) == 1:
+        assert sorted(got) == [0, 1, 2]
+    else:
+        assert 0 not in got
+
+
+def test_schedule_validation():
+    with pytest.raises(pa.PagedAttnError):
+        pa.paged_attn_schedule([10, 20], 20, 8)          # not a multiple of 16
+    with pytest.raises(pa.PagedAttnError):
+        pa.paged_attn_schedule([10, 20], 20, 16, prefix_len=32)
+    ctx = np.array([100, 100], np.int32)
+    items = np.zeros(1, np.int32)
+    n = ctypes.c_int32()
+    rc = pa._lib.paged_attn_schedule(ctx.ctypes.data_as(pa._pi32), 2, 100, 16, 0,
+                                     items.ctypes.data_as(pa._pi32), 1, ctypes.byref(n))
+    assert rc == pa.PA_EINVAL and n.value == 14
+
+
+@pytest.mark.parametrize("num_items,items,code", [(-1, 0x90000, pa.PA_EINVAL), (100, 0x90000, pa.PA_EINVAL),
+                                                  (2, 0, pa.PA_EINVAL), (2, 0x90002, pa.PA_EINVAL)])
+def test_scheduled_decode_validation(num_items, items, code):
+    p = make_pool()
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.paged_attn_decode_scheduled(p, 0x30000, 0x50000, 8, 0x60000, 2, 32, 0.1, 128, 64, items,
+                                       num_items, 0x80000, 0xA0000, 0xB0000)
+    assert e.value.code == code, pa.pa_last_error()
