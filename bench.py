@@ -49,8 +49,9 @@ KERNEL_SOURCES = {
 }
 # Split-KV partition sizes used when --partition-size is not given.  The
 # long-context pool states 512-token partitions; the other workloads state
-# none and use the size that measured fastest on them.
-DEFAULT_PARTITION = {1: 512, 2: 512, 3: 1024, 4: 1024, 5: 512}
+# none and use the size that measured fastest on them with the host-built
+# work list (the shared pool: one partition of up to 8192 tokens, no reduce).
+DEFAULT_PARTITION = {1: 512, 2: 512, 3: 1024, 4: 8192, 5: 512}
 
 
 # Prefix partition sizes (tokens) used when --prefix-partition-size is not

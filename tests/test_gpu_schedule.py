@@ -16,6 +16,7 @@ pytestmark = pytest.mark.gpu
 
 sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 
+import bench  # noqa: E402
 from oracle import compare, decode_workload  # noqa: E402
 from workloads import build_config, logical_case, page_case  # noqa: E402
 
@@ -32,6 +33,25 @@ def _gpu():
         pytest.fail("GPU tests need a visible GPU")
     yield
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_bench_launch_configurations(k):
+    """Each workload in the launch configuration bench.py times (partition
+    sizes, shared-prefix cascade, work list), against the oracle: every
+    output of the small workloads, sampled sequences of the large ones."""
+    w = build_config(k)
+    S = bench.DEFAULT_PARTITION[k]
+    L = 16 * int(w.meta.get("prefix_blocks", 0))
+    kw = dict(prefix_len=L, prefix_partition_size=bench.default_prefix_partition(k, L)) if L else {}
+    say(f"bench launch configuration {k} {w.name}: S={S} {kw}")
+    out = outputs(w, S, items=True, **kw)
+    ctx = w.context_lens
+    seqs = None if k <= 3 else sorted({0, int(np.argmax(ctx)), int(np.argmin(ctx)), w.batch // 2,
+                                       w.batch - 1})
+    rep = compare(out if seqs is None else out[seqs], decode_workload(w, seqs=seqs)[0])
+    say(f"bench configuration {k} vs oracle: {rep}")
+    assert rep.passed
 
 
 def outputs(w, S=None, items=None, **kw):
