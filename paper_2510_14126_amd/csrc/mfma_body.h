@@ -653,8 +653,8 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
 // normalises its rows and writes them as bf16.
 constexpr int kExtendRowsPerWg = 16 * kWaves;
 constexpr int kExtendRing = 6;                  // blocks whose quarter is in flight per wavefront (even)
-constexpr int kExtendLdsBytes = 4 * kPrefixStageBytes;   // two stages of a block pair
-constexpr int kExtendIdRegs = kExtendMaxTokens / (16 * 64);   // block ids per lane, 64 per register
+constexpr int kExtendIdOffset = 4 * kPrefixStageBytes;   // after two stages of a block pair
+constexpr int kExtendLdsBytes = kExtendIdOffset + kExtendMaxTokens / 16 * 4;   // + the block ids
 
 template <int G>
 __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_index, lds_u8_t* smem) {
@@ -686,23 +686,17 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
   const int vis_max = first + last_row / G + 1;
   const int nblk = (vis_max + 15) >> 4;
 
-  // Block ids of the stream, 64 per register (lane l: blocks l, l+64, ...).
-  int idc[kExtendIdRegs];
-  const int32_t* bt = p.block_tables + (size_t)b * p.bt_stride;
-#pragma unroll
-  for (int r = 0; r < kExtendIdRegs; ++r) {
-    const int j = 64 * r + lane;
-    const int raw = j < nblk ? bt[j] : 0;
-    idc[r] = min(max(raw, 0), p.num_blocks - 1);
+  // Block ids of the stream, clamped into the pool, staged once in LDS
+  // (at most kExtendMaxTokens / 16 of them); each is read back as a
+  // broadcast when its block is loaded.
+  lds_i32_t* ids = reinterpret_cast<lds_i32_t*>(smem + kExtendIdOffset);
+  {
+    const int32_t* bt = p.block_tables + (size_t)b * p.bt_stride;
+    for (int j = threadIdx.x; j < nblk; j += 64 * kWaves)
+      ids[j] = min(max(bt[j], 0), p.num_blocks - 1);
+    __syncthreads();
   }
-  auto block_id = [&](int i) {
-    const int r = i >> 6;
-    int v = idc[0];
-#pragma unroll
-    for (int k = 1; k < kExtendIdRegs; ++k)
-      if (r == k) v = idc[k];
-    return __builtin_amdgcn_readlane(v, i & 63);
-  };
+  auto block_id = [&](int i) { return __builtin_amdgcn_readfirstlane(ids[i]); };
 
   // Column n is row R = row0 + n: chunk token R / G, query head g*G + R % G.
   uint4 qb[1][4];

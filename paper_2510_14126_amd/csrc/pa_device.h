@@ -44,6 +44,7 @@ constexpr int kBufferDescWord3 = 0x00020000;
 // LDS (address space 3) pointer types.
 typedef __attribute__((address_space(3))) uint8_t lds_u8_t;
 typedef __attribute__((address_space(3))) float lds_f32_t;
+typedef __attribute__((address_space(3))) int32_t lds_i32_t;
 
 // ---- cross-lane movement ---------------------------------------------------
 
