@@ -50,7 +50,7 @@ typedef __attribute__((address_space(3))) u32x4_t lds_u32x4_t;
 constexpr int kD = 128;
 constexpr int kG = 8;
 constexpr int kWaves = 4;
-constexpr int kKPitch = kD * 2 + 16;          // LDS bytes per staged K token row
+constexpr int kKPitch = kD * 2;               // LDS bytes per staged K token row (swizzled, k_stage)
 constexpr int kStageBytes = 16 * kKPitch;     // one staged K tile
 constexpr float kLazyRescale = 8.0f;
 #ifndef PA_MFMA_NBUF
@@ -293,6 +293,13 @@ __device__ __forceinline__ void tile_core2(MfmaState<1>& S, const u32x4_t (&ka0)
 // Row of the K tile that lane (q, n) supplies as A row n: token 4(n%4) + n/4.
 __device__ __forceinline__ int k_arow(int n) { return 4 * (n & 3) + (n >> 2); }
 
+// LDS byte offset of 16-byte chunk c of token row r in a staged K tile:
+// rows of 256 bytes, chunk c at position c ^ k_arow(r).  Writers (16 lanes
+// per row, chunks 0..15) and A-operand readers (lane (q, n): row k_arow(n),
+// chunk 4s+q, i.e. position (4s+q) ^ n since k_arow is its own inverse) then
+// touch 16 distinct positions per instruction, with no padding.
+__device__ __forceinline__ int k_stage(int r, int c) { return r * kKPitch + ((c ^ k_arow(r)) << 4); }
+
 // One block of a per-sequence work item: the wavefront's own K tile goes
 // through `stage` (kStageBytes of its LDS) to reach the A-operand layout;
 // V is used from the registers it was loaded into.
@@ -304,12 +311,12 @@ __device__ __forceinline__ void process_tile(MfmaState<NT>& S, const MfmaTile& T
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     const u32x4_t k = {T.k[u].x, T.k[u].y, T.k[u].z, T.k[u].w};
-    *reinterpret_cast<lds_u32x4_t*>(stage + (4 * u + q) * kKPitch + n * 16) = k;
+    *reinterpret_cast<lds_u32x4_t*>(stage + k_stage(4 * u + q, n)) = k;
   }
   u32x4_t ka[4];
 #pragma unroll
   for (int s = 0; s < 4; ++s)
-    ka[s] = *reinterpret_cast<const lds_u32x4_t*>(stage + k_arow(n) * kKPitch + (4 * s + q) * 16);
+    ka[s] = *reinterpret_cast<const lds_u32x4_t*>(stage + k_stage(k_arow(n), 4 * s + q));
   tile_core<TAIL, NT>(S, ka, T.v, qb, valid, limit, q, scale_log2);
 }
 
@@ -484,7 +491,7 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
 // lse = -inf when it attended to nothing.
 constexpr int kPrefixRowsPerWg = 16 * kWaves;
 constexpr int kPrefixRing = 4;                  // blocks whose quarter is in flight per wavefront (even)
-constexpr int kPrefixKBytes = 16 * kKPitch;     // staged K tile (A-operand reads need the pitch)
+constexpr int kPrefixKBytes = 16 * kKPitch;     // staged K tile (swizzled, k_stage)
 constexpr int kPrefixStageBytes = kPrefixKBytes + 16 * kD * 2;  // + V tile, row pitch 256
 constexpr int kPrefixLdsBytes = 4 * kPrefixStageBytes;   // two stages of a block pair
 
@@ -580,7 +587,7 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
         for (int e = 0; e < 2; ++e) {
           lds_u8_t* sb = st + e * kPrefixStageBytes;
           const int s = 2 * h + e;
-          *reinterpret_cast<lds_u32x4_t*>(sb + (4 * wave + q) * kKPitch + n * 16) =
+          *reinterpret_cast<lds_u32x4_t*>(sb + k_stage(4 * wave + q, n)) =
               u32x4_t{ring[s][0].x, ring[s][0].y, ring[s][0].z, ring[s][0].w};
           *reinterpret_cast<lds_u32x4_t*>(sb + kPrefixKBytes + share_off) =
               u32x4_t{ring[s][1].x, ring[s][1].y, ring[s][1].z, ring[s][1].w};
@@ -593,8 +600,8 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
         uint4 vr0[4], vr1[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-          ka0[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_arow(n) * kKPitch + (4 * c + q) * 16);
-          ka1[c] = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + k_arow(n) * kKPitch + (4 * c + q) * 16);
+          ka0[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_stage(k_arow(n), 4 * c + q));
+          ka1[c] = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + k_stage(k_arow(n), 4 * c + q));
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -758,7 +765,7 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
         for (int e = 0; e < 2; ++e) {
           lds_u8_t* sb = st + e * kPrefixStageBytes;
           const int s = 2 * h + e;
-          *reinterpret_cast<lds_u32x4_t*>(sb + (4 * wave + q) * kKPitch + n * 16) =
+          *reinterpret_cast<lds_u32x4_t*>(sb + k_stage(4 * wave + q, n)) =
               u32x4_t{ring[s][0].x, ring[s][0].y, ring[s][0].z, ring[s][0].w};
           *reinterpret_cast<lds_u32x4_t*>(sb + kPrefixKBytes + share_off) =
               u32x4_t{ring[s][1].x, ring[s][1].y, ring[s][1].z, ring[s][1].w};
@@ -771,8 +778,8 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
         uint4 vr0[4], vr1[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-          ka0[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_arow(n) * kKPitch + (4 * c + q) * 16);
-          ka1[c] = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + k_arow(n) * kKPitch + (4 * c + q) * 16);
+          ka0[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_stage(k_arow(n), 4 * c + q));
+          ka1[c] = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + k_stage(k_arow(n), 4 * c + q));
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
