@@ -400,6 +400,9 @@ def main():
                     help="tokens per prefix partition (default: per workload, see DEFAULT_PREFIX_PARTITION)")
     ap.add_argument("--schedule", choices=["on", "off"], default="on",
                     help="run the decode over a host-built work list (non-empty items, longest first)")
+    ap.add_argument("--groups", choices=["auto", "on", "off"], default="auto",
+                    help="second level of sharing: groups of sequences (a fixer request's retries) "
+                         "that share tokens after the prefix (auto: when the workload has them)")
     ap.add_argument("--graph", action="store_true",
                     help="replay each step from a captured HIP graph (one per replica)")
     ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
@@ -441,7 +444,7 @@ def main():
               "the decode-attention path runs on a single GPU", file=sys.stderr)
         sys.exit(2)
 
-    from workloads import build_config
+    from workloads import build_config, group_starts
     t0 = time.perf_counter()
     w = build_config(args.config)
     w.partition_size = args.partition_size or DEFAULT_PARTITION.get(args.config, w.partition_size)
@@ -467,8 +470,14 @@ def main():
     if args.cascade == "off" or (args.cascade == "auto" and prefix_len == 0):
         prefix_len = 0
     pps = args.prefix_partition_size or default_prefix_partition(args.config, prefix_len)
+    group_len = 16 * int(w.meta.get("mid_blocks", 0)) if "groups" in w.meta else 0
+    if args.groups == "off" or (args.groups == "auto" and (group_len == 0 or prefix_len == 0)):
+        group_len = 0
+    if args.groups == "on" and group_len == 0:
+        raise SystemExit("--groups on: this workload has no groups sharing tokens after the prefix")
+    gkw = dict(group_start=group_starts(w), group_len=group_len) if group_len else {}
     base = PagedBatch(w, dev, prefix_len=prefix_len, prefix_partition_size=pps,
-                      schedule=args.schedule == "on")
+                      schedule=args.schedule == "on", **gkw)
     sched_host_us = None
     if base.items is not None:
         # host cost of the work list (a serving loop rebuilds it every step
@@ -476,7 +485,8 @@ def main():
         ts = []
         for _ in range(50):
             t1 = time.perf_counter()
-            binding.paged_attn_schedule(w.context_lens, base.max_ctx, base.partition_size, prefix_len)
+            binding.paged_attn_schedule(w.context_lens, base.max_ctx, base.partition_size,
+                                        prefix_len + group_len)
             ts.append(time.perf_counter() - t1)
         sched_host_us = round(1e6 * float(np.median(ts)), 1)
     reps = [(base.pool, base.q)]
@@ -492,6 +502,14 @@ def main():
 
     def decode_on(i, s):
         pool, q = reps[i % R]
+        if group_len:
+            n = 0 if base.items is None else int(base.items.numel())
+            binding.paged_attn_decode_cascade_groups(
+                pool, q, base.bt, base.bt_stride, base.ctx, base.batch, base.hq, w.scale,
+                base.max_ctx, base.partition_size, prefix_len, base.prefix_partition_size,
+                base.group_start, base.num_groups, base.max_group_size, group_len,
+                base.items if n else None, n, base.part_o, base.part_lse, s)
+            return
         if base.items is not None:
             n = int(base.items.numel())
             if prefix_len:
@@ -693,7 +711,10 @@ def main():
                    "head_dim": w.head_dim, "block_size": 16, "partition_size": base.partition_size,
                    "num_partitions": base.num_parts, "replicas_rotated": R,
                    "shared_prefix_cascade": {"prefix_len": prefix_len,
-                                             "prefix_partition_size": base.prefix_partition_size}
+                                             "prefix_partition_size": base.prefix_partition_size,
+                                             "groups": {"count": base.num_groups,
+                                                        "shared_tokens": group_len}
+                                             if group_len else None}
                    if prefix_len else None,
                    "work_list": (f"host-built, {int(base.items.numel())} non-empty items longest first"
                                  if base.items is not None else "full grid"),

@@ -232,6 +232,69 @@ int paged_attn_reduce_cascade(const float *partial_out, const float *partial_lse
                               int32_t prefix_partition_size, int32_t max_partitions, void *out,
                               void *stream);
 
+/* ---------------------------------------------------------------------------
+ * Two-level sharing: the prefix, then per group.
+ *
+ * The retries of one SQL-error-fixer request repeat the request's prompt --
+ * the schema and the failed first attempt -- and differ only in their own
+ * tail (Cortex paper, section 1 "Motivating Example"; section 2 "Cortex
+ * Benefits").  With the first attempt stored once per request as the same
+ * physical blocks in its retries' tables, the grouped cascade computes
+ * attention over it once per (request, KV head) for all the request's query
+ * rows together, as it does for the batch-wide prefix, instead of once per
+ * retry.  The result is again the same as paged_attn_decode.
+ * ------------------------------------------------------------------------- */
+
+/* Partial sizes of a grouped cascade step: as
+ * paged_attn_cascade_workspace_size, plus one partition per sequence for its
+ * group's shared tokens.  group_len: a multiple of 16 in [16, 1024] with
+ * prefix_len + group_len <= max_context_len. */
+int paged_attn_cascade_groups_workspace_size(int32_t batch, int32_t num_q_heads, int32_t head_dim,
+                                             int32_t max_context_len, int32_t partition_size,
+                                             int32_t prefix_len, int32_t prefix_partition_size,
+                                             int32_t group_len, size_t *partial_out_bytes,
+                                             size_t *partial_lse_bytes,
+                                             int32_t *max_partitions_out);
+
+/* First half of a grouped cascade step.  Besides paged_attn_decode_cascade's
+ * arguments:
+ *   group_start     device int32 [num_groups + 1], nondecreasing, from 0 to
+ *                   batch: group k is sequences group_start[k] ..
+ *                   group_start[k+1]-1; every sequence belongs to a group
+ *                   (groups of one are fine)
+ *   max_group_size  bound on the sequences of a group; max_group_size * G
+ *                   <= 64 (G = num_q_heads / num_kv_heads)
+ *   group_len       tokens after the prefix that a group's sequences share:
+ *                   table entries prefix_len/16 .. (prefix_len+group_len)/16
+ *                   - 1 are the same physical blocks for all of a group's
+ *                   sequences, and the group's first sequence holds them all
+ *                   (a shorter member attends only to its own context)
+ *   items, num_items  a work list of the per-sequence partitions after both
+ *                   shared parts (paged_attn_schedule with prefix_len +
+ *                   group_len), or items NULL: the full grid
+ * Group data on the device is clamped into the batch and the bound; a
+ * sequence in no group leaves its group partial unwritten.  head_dim 128.
+ * Follow with paged_attn_reduce_cascade_groups. */
+int paged_attn_decode_cascade_groups(const pa_kv_pool *pool, const void *q,
+                                     const int32_t *block_tables, int32_t bt_stride,
+                                     const int32_t *context_lens, int32_t batch,
+                                     int32_t num_q_heads, float scale, int32_t max_context_len,
+                                     int32_t partition_size, int32_t prefix_len,
+                                     int32_t prefix_partition_size, const int32_t *group_start,
+                                     int32_t num_groups, int32_t max_group_size, int32_t group_len,
+                                     const int32_t *items, int32_t num_items, float *partial_out,
+                                     float *partial_lse, void *stream);
+
+/* Second half of a grouped cascade step: merges, for each (b, h), the
+ * prefix partials, the group partial and the ceil((ctx_b - prefix_len -
+ * group_len) / partition_size) partials after them. */
+int paged_attn_reduce_cascade_groups(const float *partial_out, const float *partial_lse,
+                                     const int32_t *context_lens, int32_t batch,
+                                     int32_t num_q_heads, int32_t head_dim, int32_t partition_size,
+                                     int32_t prefix_len, int32_t prefix_partition_size,
+                                     int32_t group_len, int32_t max_partitions, void *out,
+                                     void *stream);
+
 /* Index-trace variant of paged_attn_decode, for verifying block-table and
  * context-length handling.  It runs the same gather code and, in addition,
  * records for every work item (partition p, sequence b, KV head g) the

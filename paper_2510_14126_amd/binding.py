@@ -48,6 +48,14 @@ SIGNATURES = {
     "pa_stream_copy": (_c_int, [_vp, _vp, _sz, _vp]),
     "paged_attn_append_kv": (_c_int, [_vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp]),
     "paged_attn_schedule": (_c_int, [_pi32, _i32, _i32, _i32, _i32, _pi32, _i32, _pi32]),
+    "paged_attn_cascade_groups_workspace_size": (_c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _i32,
+                                                         _i32, ctypes.POINTER(_sz),
+                                                         ctypes.POINTER(_sz), _pi32]),
+    "paged_attn_decode_cascade_groups": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32,
+                                                  _i32, _i32, _i32, _vp, _i32, _i32, _i32, _vp, _i32,
+                                                  _vp, _vp, _vp]),
+    "paged_attn_reduce_cascade_groups": (_c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32,
+                                                  _i32, _i32, _vp, _vp]),
     "paged_attn_decode_scheduled": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32, _i32,
                                              _vp, _i32, _vp, _vp, _vp, _vp]),
     "paged_attn_decode_cascade_scheduled": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32,
@@ -275,6 +283,38 @@ def paged_attn_decode_cascade(pool: KVPool, q, block_tables, bt_stride, context_
                                           max_context_len, partition_size, prefix_len,
                                           prefix_partition_size, _ptr(partial_out),
                                           _ptr(partial_lse), _ptr(stream)))
+
+
+def paged_attn_cascade_groups_workspace_size(batch, num_q_heads, head_dim, max_context_len,
+                                             partition_size, prefix_len, prefix_partition_size,
+                                             group_len):
+    """Returns (partial_out bytes, partial_lse bytes, max_partitions)."""
+    a, b, m = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_int32()
+    _check(_lib.paged_attn_cascade_groups_workspace_size(
+        batch, num_q_heads, head_dim, max_context_len, partition_size, prefix_len,
+        prefix_partition_size, group_len, ctypes.byref(a), ctypes.byref(b), ctypes.byref(m)))
+    return a.value, b.value, m.value
+
+
+def paged_attn_decode_cascade_groups(pool: KVPool, q, block_tables, bt_stride, context_lens, batch,
+                                     num_q_heads, scale, max_context_len, partition_size,
+                                     prefix_len, prefix_partition_size, group_start, num_groups,
+                                     max_group_size, group_len, items, num_items, partial_out,
+                                     partial_lse, stream=None) -> None:
+    _check(_lib.paged_attn_decode_cascade_groups(
+        pool._handle(), _ptr(q), _ptr(block_tables), bt_stride, _ptr(context_lens), batch,
+        num_q_heads, scale, max_context_len, partition_size, prefix_len, prefix_partition_size,
+        _ptr(group_start), num_groups, max_group_size, group_len, _ptr(items), num_items,
+        _ptr(partial_out), _ptr(partial_lse), _ptr(stream)))
+
+
+def paged_attn_reduce_cascade_groups(partial_out, partial_lse, context_lens, batch, num_q_heads,
+                                     head_dim, partition_size, prefix_len, prefix_partition_size,
+                                     group_len, max_partitions, out, stream=None) -> None:
+    _check(_lib.paged_attn_reduce_cascade_groups(
+        _ptr(partial_out), _ptr(partial_lse), _ptr(context_lens), batch, num_q_heads, head_dim,
+        partition_size, prefix_len, prefix_partition_size, group_len, max_partitions, _ptr(out),
+        _ptr(stream)))
 
 
 def paged_attn_reduce_cascade(partial_out, partial_lse, context_lens, batch, num_q_heads,

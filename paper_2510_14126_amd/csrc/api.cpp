@@ -220,12 +220,14 @@ int decode_impl(const DecodeArgs& a, int32_t partition_size, void* out, float* p
 // Partition plan of a shared-prefix (cascade) step.
 struct CascadePlan {
   int32_t pre_parts, pre_tokens;  // prefix partitions and their size
+  int32_t group_parts;            // 1 with a second level of groups, else 0
+  int32_t shared_len;             // prefix_len + group_len: where the per-sequence part starts
   int32_t suf_parts, suf_tokens;  // partitions of the rest of the longest context
   int32_t stride;                 // partitions per (sequence, head)
 };
 
 int plan_cascade(int32_t max_context_len, int32_t partition_size, int32_t prefix_len,
-                 int32_t prefix_partition_size, CascadePlan* out, const char* fn) {
+                 int32_t prefix_partition_size, int32_t group_len, CascadePlan* out, const char* fn) {
   if (max_context_len < 0) return fail(PA_EINVAL, "%s: max_context_len = %d < 0", fn, max_context_len);
   if (partition_size <= 0 || partition_size % PA_BLOCK_SIZE != 0)
     return fail(PA_EINVAL, "%s: partition_size = %d is not a positive multiple of %d", fn,
@@ -240,12 +242,19 @@ int plan_cascade(int32_t max_context_len, int32_t partition_size, int32_t prefix
       prefix_partition_size % PA_BLOCK_SIZE != 0)
     return fail(PA_EINVAL, "%s: prefix_partition_size = %d not a multiple of 16 in [16, 1024]", fn,
                 prefix_partition_size);
+  if (group_len < 0 || group_len % PA_BLOCK_SIZE != 0 || group_len > 64 * PA_BLOCK_SIZE)
+    return fail(PA_EINVAL, "%s: group_len = %d not a multiple of 16 in [0, 1024]", fn, group_len);
+  if ((int64_t)prefix_len + group_len > max_context_len)
+    return fail(PA_EINVAL, "%s: prefix_len + group_len = %d exceeds max_context_len = %d", fn,
+                prefix_len + group_len, max_context_len);
   out->pre_tokens = prefix_partition_size;
   out->pre_parts = (prefix_len + prefix_partition_size - 1) / prefix_partition_size;
+  out->group_parts = group_len > 0 ? 1 : 0;
+  out->shared_len = prefix_len + group_len;
   out->suf_tokens = partition_size;
-  const int64_t rest = (int64_t)max_context_len - prefix_len;
+  const int64_t rest = (int64_t)max_context_len - out->shared_len;
   out->suf_parts = (int32_t)((rest + partition_size - 1) / partition_size);
-  const int64_t stride = (int64_t)out->pre_parts + out->suf_parts;
+  const int64_t stride = (int64_t)out->pre_parts + out->group_parts + out->suf_parts;
   out->stride = (int32_t)(stride > 0 ? stride : 1);
   return PA_OK;
 }
@@ -426,23 +435,47 @@ int paged_attn_decode_trace(const pa_kv_pool* pool, const void* q, const int32_t
                      stream, "paged_attn_decode_trace");
 }
 
-int paged_attn_cascade_workspace_size(int32_t batch, int32_t num_q_heads, int32_t head_dim,
-                                      int32_t max_context_len, int32_t partition_size,
-                                      int32_t prefix_len, int32_t prefix_partition_size,
-                                      size_t* partial_out_bytes, size_t* partial_lse_bytes,
-                                      int32_t* max_partitions_out) {
-  const char* fn = "paged_attn_cascade_workspace_size";
+namespace {
+int cascade_workspace_impl(int32_t batch, int32_t num_q_heads, int32_t head_dim,
+                           int32_t max_context_len, int32_t partition_size, int32_t prefix_len,
+                           int32_t prefix_partition_size, int32_t group_len,
+                           size_t* partial_out_bytes, size_t* partial_lse_bytes,
+                           int32_t* max_partitions_out, const char* fn) {
   if (!partial_out_bytes || !partial_lse_bytes || !max_partitions_out)
     return fail(PA_EINVAL, "%s: NULL output pointer", fn);
   if (batch < 0 || num_q_heads <= 0 || head_dim <= 0) return fail(PA_EINVAL, "%s: bad geometry", fn);
   CascadePlan cp;
-  int rc = plan_cascade(max_context_len, partition_size, prefix_len, prefix_partition_size, &cp, fn);
+  int rc = plan_cascade(max_context_len, partition_size, prefix_len, prefix_partition_size,
+                        group_len, &cp, fn);
   if (rc) return rc;
   const size_t rows = (size_t)batch * num_q_heads * cp.stride;
   *partial_out_bytes = rows * head_dim * sizeof(float);
   *partial_lse_bytes = rows * sizeof(float);
   *max_partitions_out = cp.stride;
   return PA_OK;
+}
+}  // namespace
+
+int paged_attn_cascade_workspace_size(int32_t batch, int32_t num_q_heads, int32_t head_dim,
+                                      int32_t max_context_len, int32_t partition_size,
+                                      int32_t prefix_len, int32_t prefix_partition_size,
+                                      size_t* partial_out_bytes, size_t* partial_lse_bytes,
+                                      int32_t* max_partitions_out) {
+  return cascade_workspace_impl(batch, num_q_heads, head_dim, max_context_len, partition_size,
+                                prefix_len, prefix_partition_size, 0, partial_out_bytes,
+                                partial_lse_bytes, max_partitions_out,
+                                "paged_attn_cascade_workspace_size");
+}
+
+int paged_attn_cascade_groups_workspace_size(int32_t batch, int32_t num_q_heads, int32_t head_dim,
+                                             int32_t max_context_len, int32_t partition_size,
+                                             int32_t prefix_len, int32_t prefix_partition_size,
+                                             int32_t group_len, size_t* partial_out_bytes,
+                                             size_t* partial_lse_bytes, int32_t* max_partitions_out) {
+  return cascade_workspace_impl(batch, num_q_heads, head_dim, max_context_len, partition_size,
+                                prefix_len, prefix_partition_size, group_len, partial_out_bytes,
+                                partial_lse_bytes, max_partitions_out,
+                                "paged_attn_cascade_groups_workspace_size");
 }
 
 namespace {
@@ -452,23 +485,36 @@ int cascade_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tab
                  int32_t num_q_heads, float scale, int32_t max_context_len,
                  int32_t partition_size, int32_t prefix_len, int32_t prefix_partition_size,
                  float* partial_out, float* partial_lse, void* stream, const char* fn,
-                 bool scheduled, const int32_t* items, int32_t num_items) {
+                 bool scheduled, const int32_t* items, int32_t num_items,
+                 const int32_t* group_start = nullptr, int32_t num_groups = 0,
+                 int32_t max_group_size = 0, int32_t group_len = 0) {
   const DecodeArgs a{pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
                      max_context_len};
   int32_t group = 0;
   int rc = validate_decode(a, &group, fn);
   if (rc) return rc;
   CascadePlan cp;
-  rc = plan_cascade(max_context_len, partition_size, prefix_len, prefix_partition_size, &cp, fn);
+  rc = plan_cascade(max_context_len, partition_size, prefix_len, prefix_partition_size, group_len,
+                    &cp, fn);
   if (rc) return rc;
-  if (prefix_len > 0 && pool->head_dim != 128)
-    return fail(PA_EUNSUPPORTED, "%s: the shared-prefix pass needs head_dim 128", fn);
+  if ((prefix_len > 0 || group_len > 0) && pool->head_dim != 128)
+    return fail(PA_EUNSUPPORTED, "%s: the shared passes need head_dim 128", fn);
+  if (group_len > 0) {
+    if (num_groups < 1 || num_groups > (batch > 0 ? batch : 1))
+      return fail(PA_EINVAL, "%s: num_groups = %d outside [1, batch]", fn, num_groups);
+    if (max_group_size < 1 || (int64_t)max_group_size * group > 64)
+      return fail(PA_EINVAL, "%s: max_group_size = %d: groups of 1 .. %d sequences at %d heads per "
+                  "KV head", fn, max_group_size, 64 / group, group);
+    if (batch > 0 && (!group_start || !aligned(group_start, 4)))
+      return fail(PA_EINVAL, "%s: group_start is NULL or not 4-byte aligned", fn);
+  }
   const int64_t rows = (int64_t)batch * num_q_heads;
   // Upper bound on the fused grid: a prefix workgroup covers at least 16 query
   // rows of one KV head, a suffix workgroup one (sequence, KV head) pair.
   const int64_t g_pre = (int64_t)cp.pre_parts * ((rows / pool->num_kv_heads + 15) / 16) * pool->num_kv_heads;
   const int64_t g_suf = (int64_t)cp.suf_parts * batch * pool->num_kv_heads;
-  if (g_pre + g_suf > 0x7fffffffLL)
+  const int64_t g_grp = group_len > 0 ? (int64_t)num_groups * pool->num_kv_heads : 0;
+  if (g_pre + g_grp + g_suf > 0x7fffffffLL)
     return fail(PA_EINVAL, "%s: grid too large", fn);
   if (scheduled) {
     rc = validate_items(items, num_items, (int64_t)cp.suf_parts * batch, fn);
@@ -491,11 +537,18 @@ int cascade_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tab
   pp.num_kv_heads = pool->num_kv_heads;
   pp.num_q_heads = num_q_heads;
   pp.batch = batch;
+  pp.bt_stride = bt_stride;
   pp.prefix_len = prefix_len;
   pp.part_tokens = cp.pre_tokens;
   pp.prefix_parts = cp.pre_parts;
   pp.part_stride = cp.stride;
   pp.max_ctx = max_context_len;
+  if (group_len > 0) {
+    pp.group_start = group_start;
+    pp.num_groups = num_groups;
+    pp.max_group_size = max_group_size;
+    pp.group_len = group_len;
+  }
   pp.scale_log2 = scale * 1.4426950408889634f;
   pa::DecodeParams p = decode_params(a);
   p.part_o = partial_out;
@@ -503,8 +556,8 @@ int cascade_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tab
   p.part_tokens = cp.suf_tokens;
   p.num_parts = cp.suf_parts;
   p.item_order = item_order_for(cp.suf_parts);
-  p.token_offset = prefix_len;
-  p.part_offset = cp.pre_parts;
+  p.token_offset = cp.shared_len;
+  p.part_offset = cp.pre_parts + cp.group_parts;
   p.part_stride = cp.stride;
   p.write_partials = 1;
   p.trace_tiles = cp.suf_tokens / PA_BLOCK_SIZE;
@@ -518,7 +571,7 @@ int cascade_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tab
     if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
     return PA_OK;
   }
-  if (cp.suf_parts > 0) {  // no prefix (head_dim 64 requires prefix_len 0)
+  if (cp.suf_parts > 0) {  // no shared pass (head_dim 64 requires prefix_len 0, no groups)
     hipError_t e = launch_decode(p, pool, group, false, stream);
     if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
   }
@@ -556,6 +609,23 @@ int paged_attn_decode_cascade_scheduled(const pa_kv_pool* pool, const void* q,
                       max_context_len, partition_size, prefix_len, prefix_partition_size,
                       partial_out, partial_lse, stream, "paged_attn_decode_cascade_scheduled", true,
                       items, num_items);
+}
+
+int paged_attn_decode_cascade_groups(const pa_kv_pool* pool, const void* q,
+                                     const int32_t* block_tables, int32_t bt_stride,
+                                     const int32_t* context_lens, int32_t batch, int32_t num_q_heads,
+                                     float scale, int32_t max_context_len, int32_t partition_size,
+                                     int32_t prefix_len, int32_t prefix_partition_size,
+                                     const int32_t* group_start, int32_t num_groups,
+                                     int32_t max_group_size, int32_t group_len, const int32_t* items,
+                                     int32_t num_items, float* partial_out, float* partial_lse,
+                                     void* stream) {
+  const char* fn = "paged_attn_decode_cascade_groups";
+  if (group_len <= 0) return fail(PA_EINVAL, "%s: group_len = %d <= 0", fn, group_len);
+  return cascade_impl(pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
+                      max_context_len, partition_size, prefix_len, prefix_partition_size,
+                      partial_out, partial_lse, stream, fn, items != nullptr, items, num_items,
+                      group_start, num_groups, max_group_size, group_len);
 }
 
 int paged_attn_decode_scheduled(const pa_kv_pool* pool, const void* q, const int32_t* block_tables,
@@ -689,6 +759,29 @@ int paged_attn_reduce_cascade(const float* partial_out, const float* partial_lse
   const int32_t pre_parts = (prefix_len + prefix_partition_size - 1) / prefix_partition_size;
   return reduce_impl(partial_out, partial_lse, context_lens, batch, num_q_heads, head_dim,
                      partition_size, max_partitions, pre_parts, prefix_len, out, stream, fn);
+}
+
+int paged_attn_reduce_cascade_groups(const float* partial_out, const float* partial_lse,
+                                     const int32_t* context_lens, int32_t batch,
+                                     int32_t num_q_heads, int32_t head_dim, int32_t partition_size,
+                                     int32_t prefix_len, int32_t prefix_partition_size,
+                                     int32_t group_len, int32_t max_partitions, void* out,
+                                     void* stream) {
+  const char* fn = "paged_attn_reduce_cascade_groups";
+  if (prefix_len < 0 || prefix_len % PA_BLOCK_SIZE != 0)
+    return fail(PA_EINVAL, "%s: prefix_len = %d is not a non-negative multiple of %d", fn,
+                prefix_len, PA_BLOCK_SIZE);
+  if (prefix_partition_size < PA_BLOCK_SIZE || prefix_partition_size > 64 * PA_BLOCK_SIZE ||
+      prefix_partition_size % PA_BLOCK_SIZE != 0)
+    return fail(PA_EINVAL, "%s: prefix_partition_size = %d not a multiple of 16 in [16, 1024]", fn,
+                prefix_partition_size);
+  if (group_len <= 0 || group_len % PA_BLOCK_SIZE != 0 || group_len > 64 * PA_BLOCK_SIZE)
+    return fail(PA_EINVAL, "%s: group_len = %d not a multiple of 16 in [16, 1024]", fn, group_len);
+  // every sequence has the prefix partitions and its group's partition
+  const int32_t shared_parts = (prefix_len + prefix_partition_size - 1) / prefix_partition_size + 1;
+  return reduce_impl(partial_out, partial_lse, context_lens, batch, num_q_heads, head_dim,
+                     partition_size, max_partitions, shared_parts, prefix_len + group_len, out,
+                     stream, fn);
 }
 
 int paged_attn_extend(const pa_kv_pool* pool, const void* q, const int32_t* q_start, int32_t total_q,

@@ -1,7 +1,9 @@
 // One-launch shared-prefix (cascade) step: some workgroups run the
-// shared-prefix pass (matrix-core tiles over all query rows), the others run
-// the per-sequence decode over the tokens after the prefix.  Both write
-// disjoint (o, lse) partials, so they need no synchronisation.  The two kinds
+// shared-prefix pass (matrix-core tiles over all query rows) and, with a
+// second level, the pass over each group's shared tokens (tiles over the
+// group's rows); the others run the per-sequence decode over the tokens
+// after what is shared.  All write disjoint (o, lse) partials, so they need
+// no synchronisation.  Shared and per-sequence work
 // alternate in runs of num_kv_heads workgroups, so every CU holds some of
 // each at once: the L2-fed prefix work overlaps the HBM-fed per-sequence work
 // instead of preceding it, and workgroup i still serves KV head
@@ -26,28 +28,36 @@ constexpr int kCascadeValuNbuf = 2;
 
 template <int G>
 __global__ void __launch_bounds__(64 * mfma::kWaves) __attribute__((amdgpu_waves_per_eu(2, 8)))
-cascade_kernel(const PrefixParams pp, const DecodeParams dp, int prefix_runs, int decode_runs) {
+cascade_kernel(const PrefixParams pp, const DecodeParams dp, int prefix_runs, int group_runs,
+               int decode_runs) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[kCascadeLds];
   lds_u8_t* lds = (lds_u8_t*)smem;
-  // Run r = blockIdx / Hkv: while both kinds remain, even runs are prefix
-  // runs and odd runs decode runs; then the longer kind continues alone.
+  // Run r = blockIdx / Hkv: while both kinds remain, even runs are shared
+  // runs (the prefix partitions, then the groups) and odd runs decode runs;
+  // then the longer kind continues alone.
   const int hkv = dp.num_kv_heads;
   const int run = blockIdx.x / hkv;
   const int g = blockIdx.x - run * hkv;
-  const int both = min(prefix_runs, decode_runs);
-  bool prefix;
+  const int shared_runs = prefix_runs + group_runs;
+  const int both = min(shared_runs, decode_runs);
+  bool shared;
   int idx;
   if (run < 2 * both) {
-    prefix = (run & 1) == 0;
+    shared = (run & 1) == 0;
     idx = run >> 1;
   } else {
-    prefix = prefix_runs > decode_runs;
+    shared = shared_runs > decode_runs;
     idx = both + (run - 2 * both);
   }
+  if (shared) {
+    if (idx < prefix_runs)
+      mfma::prefix_mfma_body<G>(pp, idx * hkv + g, lds);
+    else
+      mfma::group_mfma_body<G>(pp, (idx - prefix_runs) * hkv + g, lds);
+    return;
+  }
   const int wg = idx * hkv + g;
-  if (prefix) {
-    mfma::prefix_mfma_body<G>(pp, wg, lds);
-  } else if constexpr (G == 4) {
+  if constexpr (G == 4) {
     valu::decode_valu_body<128, 4, PA_VALU_WAVES, kCascadeValuNbuf, false>(dp, wg, lds);
   } else {
     mfma::decode_mfma_body<false>(dp, wg, lds);
@@ -64,16 +74,17 @@ hipError_t launch_cascade(const PrefixParams& pp, const DecodeParams& dp, int gr
   // fastest index of both).
   if (pp.num_kv_heads != dp.num_kv_heads) return hipErrorInvalidValue;
   const int64_t prefix_runs = (int64_t)pp.prefix_parts * row_groups;
+  const int64_t group_runs = pp.num_groups > 0 ? pp.num_groups : 0;
   const int64_t decode_runs = decode_items(dp);
-  const int64_t grid = (prefix_runs + decode_runs) * dp.num_kv_heads;
+  const int64_t grid = (prefix_runs + group_runs + decode_runs) * dp.num_kv_heads;
   if (grid == 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
   if (group == 4)
     hipLaunchKernelGGL(cascade_kernel<4>, dim3((unsigned)grid), dim3(64 * mfma::kWaves), 0, stream,
-                       pp, dp, (int)prefix_runs, (int)decode_runs);
+                       pp, dp, (int)prefix_runs, (int)group_runs, (int)decode_runs);
   else if (group == 8)
     hipLaunchKernelGGL(cascade_kernel<8>, dim3((unsigned)grid), dim3(64 * mfma::kWaves), 0, stream,
-                       pp, dp, (int)prefix_runs, (int)decode_runs);
+                       pp, dp, (int)prefix_runs, (int)group_runs, (int)decode_runs);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

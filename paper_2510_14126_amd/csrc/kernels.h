@@ -67,24 +67,35 @@ __device__ __forceinline__ void decode_item(const DecodeParams& p, int wg, int& 
 }
 
 // Attention of every query row of the batch over a prefix that all
-// sequences share (same physical blocks, read from sequence 0's table).
+// sequences share (same physical blocks, read from sequence 0's table), and
+// optionally, one level down, of each group of sequences over the tokens
+// that the group shares after the prefix (read from the group's first
+// sequence's table).
 struct PrefixParams {
   const uint16_t* k_pool;
   const uint16_t* v_pool;
   const uint16_t* q;
-  const int32_t* block_tables;   // only row 0 is read
+  const int32_t* block_tables;   // [batch][bt_stride]
   const int32_t* context_lens;
-  float* part_o;                 // partitions [0, prefix_parts) of the partial buffers
+  float* part_o;                 // partitions [0, prefix_parts (+1)) of the partial buffers
   float* part_lse;
   int32_t num_blocks;
   int32_t num_kv_heads;
   int32_t num_q_heads;
   int32_t batch;
+  int32_t bt_stride;
   int32_t prefix_len;            // shared tokens (a multiple of 16)
   int32_t part_tokens;           // tokens per prefix partition (a multiple of 16)
   int32_t prefix_parts;          // ceil(prefix_len / part_tokens)
   int32_t part_stride;
   int32_t max_ctx;
+  // Second level (num_groups > 0): group k is sequences group_start[k] ..
+  // group_start[k+1]-1 (at most max_group_size of them), sharing group_len
+  // tokens after the prefix; its partial is partition prefix_parts.
+  const int32_t* group_start;    // device [num_groups + 1]
+  int32_t num_groups;
+  int32_t max_group_size;        // max_group_size * G <= 64 (one workgroup per group)
+  int32_t group_len;             // a multiple of 16, at most 1024
   float scale_log2;
 };
 

@@ -495,36 +495,44 @@ constexpr int kPrefixKBytes = 16 * kKPitch;     // staged K tile (swizzled, k_st
 constexpr int kPrefixStageBytes = kPrefixKBytes + 16 * kD * 2;  // + V tile, row pitch 256
 constexpr int kPrefixLdsBytes = 4 * kPrefixStageBytes;   // two stages of a block pair
 
+// Rows and tokens of one shared-span workgroup: rows R = row0 .. (16 per
+// wavefront) of span rows 0 .. total_rows-1, row R being sequence seq0 + R / G
+// and head g*G + R % G; tokens start .. end-1, whose block ids begin at bt;
+// the result goes to partial slot `part`; the walk over the blocks starts at
+// block `rot`.
+struct SharedSpan {
+  int seq0, total_rows, row0;
+  int start, end;
+  const int32_t* bt;
+  int part;
+  int rot;
+};
+
 template <int G>
-__device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_index, lds_u8_t* smem) {
+__device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, const SharedSpan& sp,
+                                                 lds_u8_t* smem) {
   const int lane = threadIdx.x & 63;
   const int wave = wave_uniform(threadIdx.x >> 6);
   const int q = lane >> 4;
   const int n = lane & 15;
 
-  const int total_rows = p.batch * G;
-  const int groups = (total_rows + kPrefixRowsPerWg - 1) / kPrefixRowsPerWg;
-  int wg = wg_index;
-  const int g = wg % p.num_kv_heads;
-  wg /= p.num_kv_heads;
-  const int grp = wg % groups;
-  const int part = wg / groups;
-  const int row0 = grp * kPrefixRowsPerWg + 16 * wave;   // this wavefront's tile
-
-  const int start = part * p.part_tokens;
-  const int end = min(p.prefix_len, start + p.part_tokens);
-  const int nblk = (end - start + 15) >> 4;     // 1 .. 64 for every launched partition
-  const int raw = lane < nblk ? p.block_tables[(start >> 4) + lane] : 0;
+  const int total_rows = sp.total_rows;
+  const int row0 = sp.row0 + 16 * wave;   // this wavefront's tile
+  const int start = sp.start;
+  const int end = sp.end;
+  const int part = sp.part;
+  const int nblk = (end - start + 15) >> 4;     // 1 .. 64 for every launched span
+  const int raw = lane < nblk ? sp.bt[lane] : 0;
   const int idc = min(max(raw, 0), p.num_blocks - 1);
 
-  // Column n is query row R = row0 + n: sequence R / G, head g*G + R % G.
+  // Column n is query row R = row0 + n: sequence seq0 + R / G, head g*G + R % G.
   uint4 qb[1][4];
   int ctx;
   int min_ctx;
   {
     const int R = row0 + n;
     const bool ok = R < total_rows;
-    const int bR = ok ? R / G : 0;
+    const int bR = ok ? sp.seq0 + R / G : 0;
     const uint16_t* qrow = p.q + ((size_t)bR * p.num_q_heads + g * G + R % G) * kD;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
@@ -549,10 +557,7 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
   const uint16_t* kbase = p.k_pool + (size_t)g * kTileElems;
   const uint16_t* vbase = p.v_pool + (size_t)g * kTileElems;
 
-  // The workgroups of a KV head walk the partition from evenly spread
-  // starting blocks, so at any moment they read different blocks instead of
-  // all queueing on the L2 lines of the same one.
-  const int rot = (int)(((int64_t)grp * nblk) / groups) % nblk;
+  const int rot = sp.rot;
   auto block_of = [&](int i) { const int j = i + rot; return j >= nblk ? j - nblk : j; };
   auto load = [&](uint4 (&dst)[2], int i) {
     const bool ok = i < nblk;
@@ -632,7 +637,7 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
   const float inv = lcol > 0.f ? 1.0f / lcol : 0.f;
   if (q == 0 && row0 + n < total_rows) {
     const int R = row0 + n;
-    const size_t row = ((size_t)(R / G) * p.num_q_heads + g * G + R % G) * p.part_stride + part;
+    const size_t row = ((size_t)(sp.seq0 + R / G) * p.num_q_heads + g * G + R % G) * p.part_stride + part;
     p.part_lse[row] = lcol > 0.f ? (S.m[0] + log2f(lcol)) * kLn2 : -__builtin_inff();
   }
 #pragma unroll
@@ -640,12 +645,66 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
     const int R = row0 + 4 * q + r;
     const float f = column_value(inv, q, r);
     if (R < total_rows) {
-      const size_t row = ((size_t)(R / G) * p.num_q_heads + g * G + R % G) * p.part_stride + part;
+      const size_t row =
+          ((size_t)(sp.seq0 + R / G) * p.num_q_heads + g * G + R % G) * p.part_stride + part;
       float4* po = reinterpret_cast<float4*>(p.part_o + row * kD + 8 * n);
       po[0] = make_float4(S.o[0][0][r] * f, S.o[0][1][r] * f, S.o[0][2][r] * f, S.o[0][3][r] * f);
       po[1] = make_float4(S.o[0][4][r] * f, S.o[0][5][r] * f, S.o[0][6][r] * f, S.o[0][7][r] * f);
     }
   }
+}
+
+// The batch-wide prefix: partition `part` of the prefix against row group
+// `grp` (64 rows) of all B*G query rows of KV head g.
+template <int G>
+__device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_index, lds_u8_t* smem) {
+  const int total_rows = p.batch * G;
+  const int groups = (total_rows + kPrefixRowsPerWg - 1) / kPrefixRowsPerWg;
+  int wg = wg_index;
+  const int g = wg % p.num_kv_heads;
+  wg /= p.num_kv_heads;
+  const int grp = wg % groups;
+  const int part = wg / groups;
+  SharedSpan sp;
+  sp.seq0 = 0;
+  sp.total_rows = total_rows;
+  sp.row0 = grp * kPrefixRowsPerWg;
+  sp.start = part * p.part_tokens;
+  sp.end = min(p.prefix_len, sp.start + p.part_tokens);
+  sp.bt = p.block_tables + (sp.start >> 4);
+  sp.part = part;
+  // The workgroups of a KV head walk the partition from evenly spread
+  // starting blocks, so at any moment they read different blocks instead of
+  // all queueing on the L2 lines of the same one.
+  const int nblk = (sp.end - sp.start + 15) >> 4;
+  sp.rot = (int)(((int64_t)grp * nblk) / groups) % nblk;
+  shared_span_body<G>(p, g, sp, smem);
+}
+
+// The second level: group k's rows (its sequences x G heads of KV head g,
+// at most 64) against the group_len tokens the group shares after the
+// prefix, one partition written to slot prefix_parts.
+template <int G>
+__device__ __forceinline__ void group_mfma_body(const PrefixParams& p, int wg_index, lds_u8_t* smem) {
+  const int g = wg_index % p.num_kv_heads;
+  const int k = wg_index / p.num_kv_heads;
+  // device data: clamped into the batch and the stated bound
+  int s0 = p.group_start[k];
+  s0 = s0 < 0 ? 0 : (s0 > p.batch ? p.batch : s0);
+  int s1 = p.group_start[k + 1];
+  s1 = s1 < s0 ? s0 : (s1 > p.batch ? p.batch : s1);
+  s1 = min(s1, s0 + p.max_group_size);
+  if (s1 == s0) return;                        // whole workgroup: an empty group
+  SharedSpan sp;
+  sp.seq0 = s0;
+  sp.total_rows = (s1 - s0) * G;
+  sp.row0 = 0;
+  sp.start = p.prefix_len;
+  sp.end = p.prefix_len + p.group_len;
+  sp.bt = p.block_tables + (size_t)s0 * p.bt_stride + (sp.start >> 4);
+  sp.part = p.prefix_parts;
+  sp.rot = 0;
+  shared_span_body<G>(p, g, sp, smem);
 }
 
 // Causal attention of a chunk of new tokens over its sequence's paged

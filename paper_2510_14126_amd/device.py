@@ -24,7 +24,8 @@ def _dev(a: np.ndarray, device) -> torch.Tensor:
 class PagedBatch:
     def __init__(self, w, device="cuda:0", partition_size: int | None = None,
                  register_blocks: bool = True, k_pool=None, v_pool=None,
-                 prefix_len: int = 0, prefix_partition_size: int = 256, schedule: bool = False):
+                 prefix_len: int = 0, prefix_partition_size: int = 256, schedule: bool = False,
+                 group_start=None, group_len: int = 0):
         self.w = w
         self.device = torch.device(device)
         self.partition_size = w.partition_size if partition_size is None else partition_size
@@ -42,7 +43,18 @@ class PagedBatch:
             self.register_placement()
         self.prefix_len = prefix_len
         self.prefix_partition_size = prefix_partition_size
-        if prefix_len:
+        # second level: groups of consecutive sequences sharing group_len tokens after the prefix
+        self.group_len = group_len
+        self.group_start = None
+        if group_len:
+            starts = np.ascontiguousarray(group_start, dtype=np.int32)
+            self.num_groups = int(starts.size - 1)
+            self.max_group_size = int(np.diff(starts).max()) if self.num_groups else 1
+            self.group_start = torch.from_numpy(starts).to(self.device)
+            ob, lb, self.num_parts = binding.paged_attn_cascade_groups_workspace_size(
+                self.batch, self.hq, self.d, self.max_ctx, self.partition_size, prefix_len,
+                prefix_partition_size, group_len)
+        elif prefix_len:
             ob, lb, self.num_parts = binding.paged_attn_cascade_workspace_size(
                 self.batch, self.hq, self.d, self.max_ctx, self.partition_size, prefix_len,
                 prefix_partition_size)
@@ -55,7 +67,7 @@ class PagedBatch:
         self.items = None
         if schedule:
             self.set_items(binding.paged_attn_schedule(w.context_lens, self.max_ctx,
-                                                       self.partition_size, prefix_len))
+                                                       self.partition_size, prefix_len + group_len))
 
     def set_items(self, items) -> None:
         """Run the per-sequence partitions from a host work list (see paged_attn_schedule)."""
@@ -78,6 +90,14 @@ class PagedBatch:
         return int(self.w.block_tables.shape[1])
 
     def decode(self, stream=None, out=None) -> None:
+        if self.group_len:
+            n = 0 if self.items is None else int(self.items.numel())
+            binding.paged_attn_decode_cascade_groups(
+                self.pool, self.q, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,
+                self.w.scale, self.max_ctx, self.partition_size, self.prefix_len,
+                self.prefix_partition_size, self.group_start, self.num_groups, self.max_group_size,
+                self.group_len, self.items if n else None, n, self.part_o, self.part_lse, stream)
+            return
         if self.items is not None:
             n = int(self.items.numel())
             if self.prefix_len:
@@ -103,6 +123,12 @@ class PagedBatch:
                                   stream)
 
     def reduce(self, stream=None, out=None) -> None:
+        if self.group_len:
+            binding.paged_attn_reduce_cascade_groups(
+                self.part_o, self.part_lse, self.ctx, self.batch, self.hq, self.d,
+                self.partition_size, self.prefix_len, self.prefix_partition_size, self.group_len,
+                self.num_parts, self.out if out is None else out, stream)
+            return
         if self.prefix_len:
             binding.paged_attn_reduce_cascade(
                 self.part_o, self.part_lse, self.ctx, self.batch, self.hq, self.d,
@@ -115,7 +141,7 @@ class PagedBatch:
 
     @property
     def needs_reduce(self) -> bool:
-        return bool(self.prefix_len) or self.num_parts > 1
+        return bool(self.prefix_len or self.group_len) or self.num_parts > 1
 
     def run(self, stream=None) -> None:
         """One decode step: split-KV (or cascade) decode, then the merge."""

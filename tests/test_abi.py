@@ -27,7 +27,7 @@ def declared_functions():
 
 def test_header_and_library_agree():
     names = declared_functions()
-    assert len(names) == 25, names
+    assert len(names) == 28, names
     lib = pa.library()
     for n in names:
         assert hasattr(lib, n), f"library does not export {n}"
@@ -352,3 +352,37 @@ def test_scheduled_decode_validation(num_items, items, code):
         pa.paged_attn_decode_scheduled(p, 0x30000, 0x50000, 8, 0x60000, 2, 32, 0.1, 128, 64, items,
                                        num_items, 0x80000, 0xA0000, 0xB0000)
     assert e.value.code == code, pa.pa_last_error()
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(group_len=24), "EINVAL"),                   # not a multiple of 16
+    (dict(group_len=2048), "EINVAL"),                 # longer than 1024
+    (dict(group_len=0), "EINVAL"),                    # the grouped call needs group tokens
+    (dict(num_groups=0), "EINVAL"),
+    (dict(num_groups=3), "EINVAL"),                   # more groups than sequences
+    (dict(max_group_size=17), "EINVAL"),              # 17 x 4 rows > 64
+    (dict(max_group_size=0), "EINVAL"),
+    (dict(group_start=None), "EINVAL"),
+    (dict(group_start=0x70002), "EINVAL"),            # misaligned
+    (dict(prefix_len=96, group_len=48), "EINVAL"),    # past max_context_len = 128
+])
+def test_grouped_cascade_validation(kw, code):
+    args = dict(prefix_len=64, group_len=32, group_start=0x70000, num_groups=2, max_group_size=2)
+    args.update(kw)
+    p = make_pool()
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.paged_attn_decode_cascade_groups(p, 0x30000, 0x50000, 8, 0x60000, 2, 32, 0.1, 128, 64,
+                                            args["prefix_len"], 64, args["group_start"],
+                                            args["num_groups"], args["max_group_size"],
+                                            args["group_len"], None, 0, 0xA0000, 0xB0000)
+    assert e.value.code == getattr(pa, "PA_" + code), pa.pa_last_error()
+
+
+def test_grouped_workspace_and_reduce_validation():
+    ob, lb, m = pa.paged_attn_cascade_groups_workspace_size(94, 32, 128, 3324, 1024, 2048, 1024, 256)
+    assert m == 2 + 1 + 1 and ob == 94 * 32 * m * 128 * 4 and lb == 94 * 32 * m * 4
+    with pytest.raises(pa.PagedAttnError):
+        pa.paged_attn_cascade_groups_workspace_size(4, 32, 128, 300, 64, 256, 64, 64)  # past 300
+    with pytest.raises(pa.PagedAttnError):
+        pa.paged_attn_reduce_cascade_groups(0xA0000, 0xB0000, 0x60000, 2, 32, 128, 64, 64, 64, 0,
+                                            4, 0x90000)

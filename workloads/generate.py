@@ -298,6 +298,26 @@ def build_config(k: int, values: bool = True) -> Workload:
     return w
 
 
+def group_starts(w: Workload) -> np.ndarray:
+    """First sequence of each group of a workload whose sequences come in
+    consecutive groups (``meta["groups"]``), plus the batch size at the end."""
+    g = np.asarray(w.meta["groups"])
+    assert np.all(np.diff(g) >= 0), "groups must be consecutive"
+    return np.concatenate([[0], np.flatnonzero(np.diff(g)) + 1, [g.size]]).astype(np.int32)
+
+
+def grouped_case(seed: int, hq: int, hkv: int, d: int, prefix_tokens: int, group_sizes,
+                 mid_tokens: int, suffix_lens) -> Workload:
+    """A small stage batch with two levels of sharing: all sequences share
+    ``prefix_tokens``, and the sequences of each group (consecutive, sizes
+    ``group_sizes``) share ``mid_tokens`` more; random N(0,1) bf16 values."""
+    rng = np.random.default_rng(seed)
+    groups = np.repeat(np.arange(len(group_sizes)), group_sizes)
+    w = _stage_with_prefix("grouped_case", rng, int(groups.size), hq, hkv, d, prefix_tokens,
+                           np.asarray(suffix_lens), mid_groups=list(groups), mid_tokens=mid_tokens)
+    return _fill_values(w, seed)
+
+
 # --------------------------------------------------------------------------
 # small cases for pins and edge tests
 # --------------------------------------------------------------------------
