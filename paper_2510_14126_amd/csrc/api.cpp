@@ -499,13 +499,13 @@ int cascade_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tab
   if (rc) return rc;
   if ((prefix_len > 0 || group_len > 0) && pool->head_dim != 128)
     return fail(PA_EUNSUPPORTED, "%s: the shared passes need head_dim 128", fn);
-  if (group_len > 0) {
-    if (num_groups < 1 || num_groups > (batch > 0 ? batch : 1))
+  if (group_len > 0 && batch > 0) {
+    if (num_groups < 1 || num_groups > batch)
       return fail(PA_EINVAL, "%s: num_groups = %d outside [1, batch]", fn, num_groups);
     if (max_group_size < 1 || (int64_t)max_group_size * group > 64)
       return fail(PA_EINVAL, "%s: max_group_size = %d: groups of 1 .. %d sequences at %d heads per "
                   "KV head", fn, max_group_size, 64 / group, group);
-    if (batch > 0 && (!group_start || !aligned(group_start, 4)))
+    if (!group_start || !aligned(group_start, 4))
       return fail(PA_EINVAL, "%s: group_start is NULL or not 4-byte aligned", fn);
   }
   const int64_t rows = (int64_t)batch * num_q_heads;

@@ -386,3 +386,9 @@ def test_grouped_workspace_and_reduce_validation():
     with pytest.raises(pa.PagedAttnError):
         pa.paged_attn_reduce_cascade_groups(0xA0000, 0xB0000, 0x60000, 2, 32, 128, 64, 64, 64, 0,
                                             4, 0x90000)
+
+
+def test_grouped_cascade_empty_batch_is_a_no_op():
+    p = make_pool()
+    pa.paged_attn_decode_cascade_groups(p, 0, 0, 8, 0, 0, 32, 0.1, 128, 64, 64, 64, None, 0, 0, 32,
+                                        None, 0, None, None)
