@@ -13,8 +13,9 @@
 //    dims 8n .. 8n+7, of both tiles.
 //  * S^T = K Q^T with v_mfma_f32_16x16x32_bf16: A = K rows (16 tokens x 32
 //    dims per instruction, 4 instructions for D = 128) read back from an LDS
-//    copy of the K tile (row pitch 272 bytes: the 16 rows of a column fall in
-//    distinct banks); B = Q^T with the query rows in its 16 columns.  A row i
+//    copy of the K tile (k_stage: XOR-swizzled 256-byte rows, so writes and
+//    reads spread over the banks); B = Q^T with the query rows in its 16
+//    columns.  A row i
 //    is token 4(i%4) + i/4, so lane (q, n) receives the scores of tokens
 //    4r+q (r = 0..3) for query column n.
 //  * O += P V with v_mfma_f32_16x16x16bf16_1k, one per 8 output dims: the
