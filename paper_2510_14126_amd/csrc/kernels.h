@@ -117,8 +117,6 @@ hipError_t launch_decode_valu(const DecodeParams& p, int head_dim, int group, bo
                               hipStream_t stream);
 // MFMA split-KV decode for group size 8, head_dim 128.
 hipError_t launch_decode_mfma(const DecodeParams& p, bool trace, hipStream_t stream);
-// MFMA attention over a prefix shared by the whole batch (group 4 or 8, D 128).
-hipError_t launch_prefix_mfma(const PrefixParams& p, int group, hipStream_t stream);
 // Shared-prefix pass and per-sequence decode in one launch (head_dim 128;
 // the decode half uses VALU for group 4 and MFMA for group 8).
 hipError_t launch_cascade(const PrefixParams& pp, const DecodeParams& dp, int group,
