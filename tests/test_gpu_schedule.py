@@ -18,7 +18,7 @@ sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 
 import bench  # noqa: E402
 from oracle import compare, decode_workload  # noqa: E402
-from workloads import build_config, logical_case, page_case  # noqa: E402
+from workloads import build_config, group_starts, logical_case, page_case  # noqa: E402
 
 DEV = "cuda:0"
 
@@ -44,7 +44,9 @@ def test_bench_launch_configurations(k):
     S = bench.DEFAULT_PARTITION[k]
     L = 16 * int(w.meta.get("prefix_blocks", 0))
     kw = dict(prefix_len=L, prefix_partition_size=bench.default_prefix_partition(k, L)) if L else {}
-    say(f"bench launch configuration {k} {w.name}: S={S} {kw}")
+    if L and "groups" in w.meta and w.meta.get("mid_blocks", 0):     # as bench.py --groups auto
+        kw.update(group_start=group_starts(w), group_len=16 * int(w.meta["mid_blocks"]))
+    say(f"bench launch configuration {k} {w.name}: S={S} {sorted(kw)}")
     out = outputs(w, S, items=True, **kw)
     ctx = w.context_lens
     seqs = None if k <= 3 else sorted({0, int(np.argmax(ctx)), int(np.argmin(ctx)), w.batch // 2,
