@@ -613,6 +613,37 @@ def main():
     dec_avg = e_dec[0].elapsed_time(e_dec[1]) / K
     red_avg = e_dec[1].elapsed_time(e_dec[2]) / K if split else 0.0
 
+    # data-movement reference: the tiles the step reads (each distinct one
+    # once), in the decode's grid shape, read with no arithmetic
+    spans = base.tile_spans()
+    n_spans = int(spans.shape[0])
+    spans_dev = torch.from_numpy(spans).to(dev)
+    sink = torch.empty(max(1, n_spans * w.num_kv_heads * 4), dtype=torch.int32, device=dev)
+    gather_us = {}
+    for nif in (2, 4):
+        for i in range(3):
+            base.gather_tiles(spans_dev, n_spans, sink, sh, reps[i % R][0], nif)
+        torch.cuda.synchronize()
+        e_dec[0].record(stream)
+        for i in range(K):
+            base.gather_tiles(spans_dev, n_spans, sink, sh, reps[i % R][0], nif)
+        e_dec[1].record(stream)
+        torch.cuda.synchronize()
+        gather_us[nif] = 1e3 * e_dec[0].elapsed_time(e_dec[1]) / K
+    best_nif = min(gather_us, key=gather_us.get)
+    gather_avg = gather_us[best_nif] / 1e3
+    tiles_read = int(sum((int(e) - (int(s) & ~15) + 15) // 16 for _, s, e in spans)) * w.num_kv_heads
+    gather_bytes = tiles_read * 2 * 16 * w.head_dim * 2
+    gather_line = {"us_per_call": round(gather_avg * 1e3, 3), "kv_bytes": gather_bytes,
+                   "tiles_in_flight": best_nif,
+                   "us_by_tiles_in_flight": {str(k): round(v, 3) for k, v in gather_us.items()},
+                   "gbps": round(gather_bytes / (gather_avg * 1e-3) / 1e9, 1),
+                   "spans": n_spans,
+                   "decode_time_over_gather": round(dec_avg / gather_avg, 3),
+                   "note": "pa_gather_tiles: the K/V tiles of this step (each once) read in the "
+                           "decode's grid shape with no arithmetic (the faster ring depth)"}
+    log(f"gather reference: {gather_line}")
+
     # hot: one replica, same loop (optional)
     hot = []
     for i in range(K if args.hot else 0):
@@ -739,6 +770,7 @@ def main():
                      "kernel": kernel_display_name(w, kern),
                      "launch": "decode call (all kernels it launches)",
                      "bytes_per_launch": int(alg_bytes)},
+        "gather_reference": gather_line,
         "append_kv": append_line,
         "extend": extend_line,
         "cpu_baseline": cpu,

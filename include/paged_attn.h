@@ -434,13 +434,39 @@ int paged_attn_extend(const pa_kv_pool *pool, const void *q, const int32_t *q_st
                       void *stream);
 
 /* ---------------------------------------------------------------------------
- * Measurement helper.
+ * Measurement helpers.
  * ------------------------------------------------------------------------- */
 
 /* Plain device-to-device copy of `bytes` (a multiple of 16; both pointers
  * 16-byte aligned) with a streaming kernel; used to calibrate hardware
  * traffic counters and the achievable HBM bandwidth. */
 int pa_stream_copy(const void *src, void *dst, size_t bytes, void *stream);
+
+/* Data-movement reference for a decode: reads the K and V tiles of num_spans
+ * token spans for every KV head of the pool, with no arithmetic, in the
+ * grid a decode launch uses (one workgroup of four wavefronts per (span,
+ * KV head), the head fastest, the span's 16-token blocks dealt round-robin
+ * to the wavefronts, tiles_in_flight tiles of K and V in flight per
+ * wavefront: 2 suits short spans, 4 long ones).  The
+ * time of one call over the tiles that a decode step reads is what that
+ * access pattern costs on the memory system alone, the reference for the
+ * decode kernels' own time.  Like pa_stream_copy it is a measurement helper
+ * and computes nothing of the method.
+ *   block_tables  device int32 [batch][bt_stride]
+ *   spans         device int32 [num_spans][3]: sequence b, first token,
+ *                 end token; tokens [first, end) of sequence b are read
+ *                 through table row b (first rounded down to a block)
+ *   sink          device uint32 [num_spans][num_kv_heads][4]: entry
+ *                 [s][g][w] = XOR of every 32-bit word of the K and V tiles
+ *                 that wavefront w read (blocks w, w+4, ... of the span),
+ *                 so the result can be checked exactly on the host
+ * Device data is clamped into the buffers (sequence into [0, batch), tokens
+ * into [0, 16*bt_stride], ids into [0, num_blocks)): bad data reads other
+ * tiles, never out of bounds.  num_spans = 0 is a no-op.  tiles_in_flight
+ * other than 2 or 4 is PA_EINVAL. */
+int pa_gather_tiles(const pa_kv_pool *pool, const int32_t *block_tables, int32_t bt_stride,
+                    int32_t batch, const int32_t *spans, int32_t num_spans,
+                    int32_t tiles_in_flight, uint32_t *sink, void *stream);
 
 #ifdef __cplusplus
 }

@@ -46,6 +46,7 @@ SIGNATURES = {
     "paged_attn_decode_trace": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32,
                                          _i32, _vp, _vp, _vp, _vp, _i64, _vp]),
     "pa_stream_copy": (_c_int, [_vp, _vp, _sz, _vp]),
+    "pa_gather_tiles": (_c_int, [_vp, _vp, _i32, _i32, _vp, _i32, _i32, _vp, _vp]),
     "paged_attn_append_kv": (_c_int, [_vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp]),
     "paged_attn_schedule": (_c_int, [_pi32, _i32, _i32, _i32, _i32, _pi32, _i32, _pi32]),
     "paged_attn_cascade_groups_workspace_size": (_c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _i32,
@@ -256,6 +257,13 @@ def paged_attn_decode_trace(pool: KVPool, q, block_tables, bt_stride, context_le
 
 def pa_stream_copy(src, dst, nbytes, stream=None) -> None:
     _check(_lib.pa_stream_copy(_ptr(src), _ptr(dst), nbytes, _ptr(stream)))
+
+
+def pa_gather_tiles(pool: KVPool, block_tables, bt_stride, batch, spans, num_spans, sink,
+                    stream=None, tiles_in_flight: int = 2) -> None:
+    handle = pool._handle() if pool is not None else None
+    _check(_lib.pa_gather_tiles(handle, _ptr(block_tables), bt_stride, batch, _ptr(spans),
+                                num_spans, tiles_in_flight, _ptr(sink), _ptr(stream)))
 
 
 def paged_attn_append_kv(pool: KVPool, k_new, v_new, block_tables, bt_stride, context_lens, batch,

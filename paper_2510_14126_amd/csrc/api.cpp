@@ -874,4 +874,29 @@ int pa_stream_copy(const void* src, void* dst, size_t bytes, void* stream) {
   return PA_OK;
 }
 
+int pa_gather_tiles(const pa_kv_pool* pool, const int32_t* block_tables, int32_t bt_stride,
+                    int32_t batch, const int32_t* spans, int32_t num_spans,
+                    int32_t tiles_in_flight, uint32_t* sink, void* stream) {
+  const char* fn = "pa_gather_tiles";
+  if (!pool) return fail(PA_EINVAL, "%s: NULL pool", fn);
+  if (num_spans < 0) return fail(PA_EINVAL, "%s: num_spans %d < 0", fn, num_spans);
+  if (tiles_in_flight != 2 && tiles_in_flight != 4)
+    return fail(PA_EINVAL, "%s: tiles_in_flight %d must be 2 or 4", fn, tiles_in_flight);
+  if (num_spans == 0) return PA_OK;
+  if (!block_tables || !spans || !sink) return fail(PA_EINVAL, "%s: NULL pointer", fn);
+  if (!aligned(block_tables, 4) || !aligned(spans, 4) || !aligned(sink, 4))
+    return fail(PA_EINVAL, "%s: block_tables/spans/sink are not 4-byte aligned", fn);
+  if (batch < 1 || bt_stride < 1)
+    return fail(PA_EINVAL, "%s: batch %d and bt_stride %d must be >= 1", fn, batch, bt_stride);
+  if ((int64_t)num_spans * pool->num_kv_heads > 0x7fffffffLL)
+    return fail(PA_EINVAL, "%s: %d spans x %d KV heads exceed the grid limit", fn, num_spans,
+                pool->num_kv_heads);
+  hipError_t e = pa::launch_gather_tiles(pool->k, pool->v, pool->num_blocks, pool->num_kv_heads,
+                                         pool->head_dim, block_tables, bt_stride, batch, spans,
+                                         num_spans, tiles_in_flight, sink,
+                                         static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
+  return PA_OK;
+}
+
 }  // extern "C"

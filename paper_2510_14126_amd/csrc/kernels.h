@@ -165,4 +165,12 @@ hipError_t launch_append(const AppendParams& p, hipStream_t stream);
 // Streaming device copy (measurement helper).
 hipError_t launch_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
 
+// Reads the K and V tiles of token spans ([num_spans][3] int32: sequence,
+// first token, end token) for every KV head, with no arithmetic, keeping
+// tiles_in_flight (2 or 4) tiles in flight per wavefront.
+hipError_t launch_gather_tiles(const void* k_pool, const void* v_pool, int num_blocks,
+                               int num_kv_heads, int head_dim, const int32_t* block_tables,
+                               int bt_stride, int batch, const int32_t* spans, int num_spans,
+                               int tiles_in_flight, uint32_t* sink, hipStream_t stream);
+
 }  // namespace pa

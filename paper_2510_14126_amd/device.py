@@ -139,6 +139,39 @@ class PagedBatch:
                                   self.partition_size, self.num_parts,
                                   self.out if out is None else out, stream)
 
+    def tile_spans(self) -> np.ndarray:
+        """Token spans whose K/V tiles one decode step of this batch reads,
+        each distinct tile once, as int32 [n][3] (sequence, first token, end
+        token): the shared-prefix partitions through sequence 0's table, each
+        group's shared tokens through its first sequence's table, then the
+        per-sequence partitions, longest first (ties in sequence order).  For
+        ``binding.pa_gather_tiles``, the step's data movement alone."""
+        ctx = self.w.context_lens.astype(np.int64)
+        spans = []
+        L, M = self.prefix_len, self.group_len
+        if L:
+            pps = self.prefix_partition_size
+            spans += [(0, s, min(L, s + pps)) for s in range(0, L, pps)]
+        if M:
+            starts = self.group_start.cpu().numpy()
+            spans += [(int(s0), L, L + M) for s0, s1 in zip(starts[:-1], starts[1:]) if s1 > s0]
+        first = L + M
+        S = self.partition_size if self.partition_size > 0 else max(1, self.max_ctx - first)
+        tail = []
+        for b in range(self.batch):
+            for s in range(first, int(ctx[b]), S):
+                e = min(int(ctx[b]), s + S)
+                tail.append((e - s, b, s, e))
+        tail.sort(key=lambda x: -x[0])          # stable: ties keep (sequence, partition) order
+        spans += [(b, s, e) for _, b, s, e in tail]
+        return np.asarray(spans, dtype=np.int32).reshape(-1, 3)
+
+    def gather_tiles(self, spans, num_spans, sink, stream=None, pool=None,
+                     tiles_in_flight: int = 2) -> None:
+        """Read the tiles of ``spans`` (device int32 [n][3]) with no arithmetic."""
+        binding.pa_gather_tiles(self.pool if pool is None else pool, self.bt, self.bt_stride,
+                                self.batch, spans, num_spans, sink, stream, tiles_in_flight)
+
     @property
     def needs_reduce(self) -> bool:
         return bool(self.prefix_len or self.group_len) or self.num_parts > 1

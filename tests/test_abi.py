@@ -27,7 +27,7 @@ def declared_functions():
 
 def test_header_and_library_agree():
     names = declared_functions()
-    assert len(names) == 28, names
+    assert len(names) == 29, names
     lib = pa.library()
     for n in names:
         assert hasattr(lib, n), f"library does not export {n}"
@@ -192,6 +192,25 @@ def test_trace_capacity_checked():
 def test_stream_copy_validation():
     with pytest.raises(pa.PagedAttnError):
         pa.pa_stream_copy(0x1000, 0x2000, 17)
+
+
+def test_gather_tiles_validation():
+    """Host checks of the data-movement helper; no span is ever launched."""
+    p = make_pool()
+    ok = dict(block_tables=0x50000, bt_stride=4, batch=2, spans=0x60000, num_spans=3, sink=0x70000)
+    cases = [(dict(num_spans=-1), "num_spans"), (dict(block_tables=0), "NULL"),
+             (dict(spans=0), "NULL"), (dict(sink=0), "NULL"), (dict(spans=0x60002), "aligned"),
+             (dict(batch=0), "batch"), (dict(bt_stride=0), "bt_stride"),
+             (dict(num_spans=1 << 28), "grid"), (dict(tiles_in_flight=3), "tiles_in_flight"),
+             (dict(tiles_in_flight=0, num_spans=0), "tiles_in_flight")]
+    for over, msg in cases:
+        a = {**ok, **over}
+        with pytest.raises(pa.PagedAttnError) as e:
+            pa.pa_gather_tiles(p, **a)
+        assert e.value.code == pa.PA_EINVAL and msg in pa.pa_last_error(), (over, pa.pa_last_error())
+    with pytest.raises(pa.PagedAttnError):
+        pa.pa_gather_tiles(None, **ok)
+    pa.pa_gather_tiles(p, **{**ok, "num_spans": 0, "sink": 0})     # empty: no-op, no launch
 
 
 # --------------------------------------------------------------- KV append
