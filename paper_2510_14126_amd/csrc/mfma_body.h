@@ -163,19 +163,17 @@ __device__ __forceinline__ void tile_core(MfmaState<NT>& S, const u32x4_t (&ka)[
   }
 
   // Probabilities, rounded to bf16 for the matrix core; the column sum uses
-  // the same rounded values.
+  // the same rounded values, summed from the packed words by v_dot2 against
+  // (1, 1).
   short4_t pa[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     const float mref = S.m[t] == -__builtin_inff() ? 0.f : S.m[t];  // fully masked: p = 0
-    float lsum = 0.f;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const __bf16 pb = (__bf16)fast_exp2(sc[t][r] - mref);
-      lsum += (float)pb;
-      pa[t][r] = __builtin_bit_cast(short, pb);
-    }
-    S.l[t] += lsum;
+    for (int r = 0; r < 4; ++r)
+      pa[t][r] = __builtin_bit_cast(short, (__bf16)fast_exp2(sc[t][r] - mref));
+    const uint2 pw = __builtin_bit_cast(uint2, pa[t]);
+    S.l[t] = dot2_bf16(pw.y, 0x3F803F80u, dot2_bf16(pw.x, 0x3F803F80u, S.l[t]));
   }
 
   // PV: instruction j takes B = V[token 4e+q][dim 8n+j], e = 0..3: bf16 j of
@@ -258,15 +256,18 @@ __device__ __forceinline__ void tile_core2(MfmaState<1>& S, const u32x4_t (&ka0)
   }
 
   const float mref = S.m[0] == -__builtin_inff() ? 0.f : S.m[0];
+  // Probabilities rounded to bf16 (the A operand); the column sum uses the
+  // same rounded values, from the packed words by v_dot2 against (1, 1).
   bf16x8_t pa;
-  float lsum = 0.f;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const __bf16 pb = (__bf16)fast_exp2(sc[e] - mref);
-    lsum += (float)pb;
-    pa[e] = pb;
+  for (int e = 0; e < 8; ++e) pa[e] = (__bf16)fast_exp2(sc[e] - mref);
+  {
+    const u32x4_t pw = __builtin_bit_cast(u32x4_t, pa);
+    float lsum = dot2_bf16(pw[0], 0x3F803F80u, 0.f);
+    lsum = dot2_bf16(pw[1], 0x3F803F80u, lsum);
+    lsum = dot2_bf16(pw[2], 0x3F803F80u, lsum);
+    S.l[0] += dot2_bf16(pw[3], 0x3F803F80u, lsum);
   }
-  S.l[0] += lsum;
 
   uint32_t vw0[4][4], vw1[4][4];
 #pragma unroll
