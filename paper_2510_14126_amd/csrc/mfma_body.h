@@ -96,7 +96,7 @@ template <int NT>
 struct MfmaState {
   float m[NT];        // running max of query column n (log2 units), same in all groups
   float l[NT];        // this lane's share of the column sum (tokens 4q..4q+3 of each block)
-  floatx4_t o[NT][8]; // [j]: O[rows 4q+r][dim 8n + j] of each column tile
+  floatx4_t o[NT][8]; // [j]: O[rows 4q+r][dim 8n + j] (tile_core) or [dim 16j + n] (tile_core2)
 };
 
 // One 16-token block against NT column tiles that share the K and V
@@ -200,18 +200,20 @@ __device__ __forceinline__ void tile_core(MfmaState<NT>& S, const u32x4_t (&ka)[
 }
 
 // Two 16-token blocks at once against one column tile.  Lane (q, n) holds
-// the scores of tokens 4r+q (r = 0..3) of both blocks for column n and V
-// rows 4u+q of both blocks, so with the contraction index k = 8q + e standing
-// for token 4e+q of block 0 (e < 4) and token 4(e-4)+q of block 1 (e >= 4),
-// the eight probabilities are exactly the A operand and the eight V rows the
-// B operand of one v_mfma_f32_16x16x32_bf16 per 8 output dims: PV runs at the
-// full bf16 rate and the softmax bookkeeping happens once per 32 tokens.
-// valid0/valid1 and lim0/lim1 as `valid` and `limit` of tile_core, per block
-// (a block with valid = 0 contributes nothing).
+// the scores of tokens 4r+q (r = 0..3) of both blocks for column n, so with
+// the contraction index k = 8q + e standing for token 4e+q of block 0
+// (e < 4) and token 4(e-4)+q of block 1 (e >= 4), the eight probabilities
+// are exactly the A operand of one v_mfma_f32_16x16x32_bf16 per 16 output
+// dims: PV runs at the full bf16 rate and the softmax bookkeeping happens
+// once per 32 tokens.  The B operand of instruction j (output column n =
+// dim 16j + n) comes straight from the staged V tiles (vst0, vst1; layout
+// v_stage) by two transposing LDS reads, one per block; vtr is the lane's
+// v_tr offset.  valid0/valid1 and lim0/lim1 as `valid` and `limit` of
+// tile_core, per block (a block with valid = 0 contributes nothing).
 template <bool TAIL>
 __device__ __forceinline__ void tile_core2(MfmaState<1>& S, const u32x4_t (&ka0)[4],
-                                           const u32x4_t (&ka1)[4], const uint4 (&vrow0)[4],
-                                           const uint4 (&vrow1)[4], const uint4 (&qb)[1][4],
+                                           const u32x4_t (&ka1)[4], const lds_u8_t* vst0,
+                                           const lds_u8_t* vst1, int vtr, const uint4 (&qb)[1][4],
                                            int valid0, int valid1, int lim0, int lim1, int q,
                                            float scale_log2) {
   const floatx4_t z = {0.f, 0.f, 0.f, 0.f};
@@ -269,24 +271,23 @@ __device__ __forceinline__ void tile_core2(MfmaState<1>& S, const u32x4_t (&ka0)
     S.l[0] += dot2_bf16(pw[3], 0x3F803F80u, lsum);
   }
 
-  uint32_t vw0[4][4], vw1[4][4];
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const bool k0 = !(TAIL && 4 * u + q >= valid0);
-    const bool k1 = !(TAIL && 4 * u + q >= valid1);
-    vw0[u][0] = k0 ? vrow0[u].x : 0u; vw0[u][1] = k0 ? vrow0[u].y : 0u;
-    vw0[u][2] = k0 ? vrow0[u].z : 0u; vw0[u][3] = k0 ? vrow0[u].w : 0u;
-    vw1[u][0] = k1 ? vrow1[u].x : 0u; vw1[u][1] = k1 ? vrow1[u].y : 0u;
-    vw1[u][2] = k1 ? vrow1[u].z : 0u; vw1[u][3] = k1 ? vrow1[u].w : 0u;
+  // Element e of a block's B words is its token 4e + q; rows past `valid`
+  // are zeroed (their V may be anything, NaN included).
+  uint32_t m0 = 0xffffffffu, m1 = 0xffffffffu, m2 = 0xffffffffu, m3 = 0xffffffffu;
+  if constexpr (TAIL) {
+    m0 = (q < valid0 ? 0xffffu : 0u) | (q + 4 < valid0 ? 0xffff0000u : 0u);
+    m1 = (q + 8 < valid0 ? 0xffffu : 0u) | (q + 12 < valid0 ? 0xffff0000u : 0u);
+    m2 = (q < valid1 ? 0xffffu : 0u) | (q + 4 < valid1 ? 0xffff0000u : 0u);
+    m3 = (q + 8 < valid1 ? 0xffffu : 0u) | (q + 12 < valid1 ? 0xffff0000u : 0u);
   }
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
-    const int w = j >> 1;
-    const u32x4_t vb = {__builtin_amdgcn_perm(vw0[1][w], vw0[0][w], sel),
-                        __builtin_amdgcn_perm(vw0[3][w], vw0[2][w], sel),
-                        __builtin_amdgcn_perm(vw1[1][w], vw1[0][w], sel),
-                        __builtin_amdgcn_perm(vw1[3][w], vw1[2][w], sel)};
+    const int off = vtr ^ (j << 5);
+    const uint2 b0 = __builtin_bit_cast(
+        uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vst0 + off)));
+    const uint2 b1 = __builtin_bit_cast(
+        uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vst1 + off)));
+    const u32x4_t vb = {b0.x & m0, b0.y & m1, b1.x & m2, b1.y & m3};
     S.o[0][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, __builtin_bit_cast(bf16x8_t, vb), S.o[0][j],
                                                         0, 0, 0);
   }
@@ -301,6 +302,24 @@ __device__ __forceinline__ int k_arow(int n) { return 4 * (n & 3) + (n >> 2); }
 // chunk 4s+q, i.e. position (4s+q) ^ n since k_arow is its own inverse) then
 // touch 16 distinct positions per instruction, with no padding.
 __device__ __forceinline__ int k_stage(int r, int c) { return r * kKPitch + ((c ^ k_arow(r)) << 4); }
+
+// LDS byte offset of 16-byte chunk c (dims 8c .. 8c+7) of token row r in a
+// staged V tile: rows of 256 bytes, each of eight 32-byte windows (dims
+// 16w .. 16w+15) at window position w ^ (r & 7).  Writers (16 lanes per row)
+// fill whole rows; the transposing reads of tile_core2 (16 rows x one window
+// per instruction) then spread over all eight window positions.
+__device__ __forceinline__ int v_stage(int r, int c) {
+  return r * 256 + ((((c >> 1) ^ (r & 7)) << 5) | ((c & 1) << 4));
+}
+
+// Lane (q, n)'s address in a staged V tile for the transposing read of
+// window 0 (XOR j << 5 for window j): row q + 4(n/4), dims 4(n%4) .. +3.  The
+// read hands lane n of group q element n%4 of the rows addressed by lanes
+// 4k + n/4 of its group, i.e. V[token q + 4k][dim 16j + n] for k = 0..3.
+__device__ __forceinline__ int v_tr(int q, int n) {
+  const int r = q + 4 * (n >> 2);
+  return r * 256 + ((r & 7) << 5) + ((n & 3) << 3);
+}
 
 // One block of a per-sequence work item: the wavefront's own K tile goes
 // through `stage` (kStageBytes of its LDS) to reach the A-operand layout;
@@ -556,6 +575,7 @@ __device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, c
   const size_t blk_stride = (size_t)p.num_kv_heads * kTileElems;
   // This wavefront's quarter of a tile: token row 4*wave + q, chunk n.
   const int share_off = ((4 * wave + q) * kD + n * 8) * 2;
+  const int vtr = v_tr(q, n);
   const uint16_t* kbase = p.k_pool + (size_t)g * kTileElems;
   const uint16_t* vbase = p.v_pool + (size_t)g * kTileElems;
 
@@ -596,7 +616,7 @@ __device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, c
           const int s = 2 * h + e;
           *reinterpret_cast<lds_u32x4_t*>(sb + k_stage(4 * wave + q, n)) =
               u32x4_t{ring[s][0].x, ring[s][0].y, ring[s][0].z, ring[s][0].w};
-          *reinterpret_cast<lds_u32x4_t*>(sb + kPrefixKBytes + share_off) =
+          *reinterpret_cast<lds_u32x4_t*>(sb + kPrefixKBytes + v_stage(4 * wave + q, n)) =
               u32x4_t{ring[s][1].x, ring[s][1].y, ring[s][1].z, ring[s][1].w};
         }
         load(ring[(2 * h + kRing - 2) % kRing], 2 * j + kRing - 2);
@@ -604,20 +624,13 @@ __device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, c
         __syncthreads();
 
         u32x4_t ka0[4], ka1[4];
-        uint4 vr0[4], vr1[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           ka0[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_stage(k_arow(n), 4 * c + q));
           ka1[c] = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + k_stage(k_arow(n), 4 * c + q));
         }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int off = kPrefixKBytes + ((4 * u + q) * kD + n * 8) * 2;
-          const u32x4_t v0 = *reinterpret_cast<const lds_u32x4_t*>(st + off);
-          const u32x4_t v1 = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + off);
-          vr0[u] = make_uint4(v0[0], v0[1], v0[2], v0[3]);
-          vr1[u] = make_uint4(v1[0], v1[1], v1[2], v1[3]);
-        }
+        const lds_u8_t* vst0 = st + kPrefixKBytes;
+        const lds_u8_t* vst1 = st + kPrefixStageBytes + kPrefixKBytes;
         const bool has1 = 2 * j + 1 < nblk;
         const int ta = start + block_of(2 * j) * 16;
         const int tb = has1 ? start + block_of(2 * j + 1) * 16 : end;
@@ -626,15 +639,15 @@ __device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, c
         const int lim0 = min(valid0, max(ctx - ta, 0));
         const int lim1 = min(valid1, max(ctx - tb, 0));
         if (valid0 == 16 && valid1 == 16 && min_ctx - ta >= 16 && min_ctx - tb >= 16)
-          tile_core2<false>(S, ka0, ka1, vr0, vr1, qb, 16, 16, lim0, lim1, q, p.scale_log2);
+          tile_core2<false>(S, ka0, ka1, vst0, vst1, vtr, qb, 16, 16, lim0, lim1, q, p.scale_log2);
         else
-          tile_core2<true>(S, ka0, ka1, vr0, vr1, qb, valid0, valid1, lim0, lim1, q, p.scale_log2);
+          tile_core2<true>(S, ka0, ka1, vst0, vst1, vtr, qb, valid0, valid1, lim0, lim1, q, p.scale_log2);
       }
     }
   }
 
   // Normalise per row and write this partition's partials: lane (q, n)
-  // holds O[rows 4q+r][dims 8n .. 8n+7].
+  // holds O[rows 4q+r][dims 16j + n], j = 0..7.
   const float lcol = group_sum4(S.l[0]);
   const float inv = lcol > 0.f ? 1.0f / lcol : 0.f;
   if (q == 0 && row0 + n < total_rows) {
@@ -649,9 +662,9 @@ __device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, c
     if (R < total_rows) {
       const size_t row =
           ((size_t)(sp.seq0 + R / G) * p.num_q_heads + g * G + R % G) * p.part_stride + part;
-      float4* po = reinterpret_cast<float4*>(p.part_o + row * kD + 8 * n);
-      po[0] = make_float4(S.o[0][0][r] * f, S.o[0][1][r] * f, S.o[0][2][r] * f, S.o[0][3][r] * f);
-      po[1] = make_float4(S.o[0][4][r] * f, S.o[0][5][r] * f, S.o[0][6][r] * f, S.o[0][7][r] * f);
+      float* po = p.part_o + row * kD + n;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) po[16 * j] = S.o[0][j][r] * f;
     }
   }
 }
@@ -792,6 +805,7 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
   constexpr size_t kTileElems = 16 * kD;
   const size_t blk_stride = (size_t)p.num_kv_heads * kTileElems;
   const int share_off = ((4 * wave + q) * kD + n * 8) * 2;   // token row 4*wave + q, chunk n
+  const int vtr = v_tr(q, n);
   const uint16_t* kbase = p.k_pool + (size_t)g * kTileElems;
   const uint16_t* vbase = p.v_pool + (size_t)g * kTileElems;
   auto load = [&](uint4 (&dst)[2], int i) {
@@ -828,7 +842,7 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
           const int s = 2 * h + e;
           *reinterpret_cast<lds_u32x4_t*>(sb + k_stage(4 * wave + q, n)) =
               u32x4_t{ring[s][0].x, ring[s][0].y, ring[s][0].z, ring[s][0].w};
-          *reinterpret_cast<lds_u32x4_t*>(sb + kPrefixKBytes + share_off) =
+          *reinterpret_cast<lds_u32x4_t*>(sb + kPrefixKBytes + v_stage(4 * wave + q, n)) =
               u32x4_t{ring[s][1].x, ring[s][1].y, ring[s][1].z, ring[s][1].w};
         }
         load(ring[(2 * h + kRing - 2) % kRing], 2 * j + kRing - 2);
@@ -836,34 +850,27 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
         __syncthreads();
 
         u32x4_t ka0[4], ka1[4];
-        uint4 vr0[4], vr1[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           ka0[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_stage(k_arow(n), 4 * c + q));
           ka1[c] = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + k_stage(k_arow(n), 4 * c + q));
         }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int off = kPrefixKBytes + ((4 * u + q) * kD + n * 8) * 2;
-          const u32x4_t v0 = *reinterpret_cast<const lds_u32x4_t*>(st + off);
-          const u32x4_t v1 = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + off);
-          vr0[u] = make_uint4(v0[0], v0[1], v0[2], v0[3]);
-          vr1[u] = make_uint4(v1[0], v1[1], v1[2], v1[3]);
-        }
+        const lds_u8_t* vst0 = st + kPrefixKBytes;
+        const lds_u8_t* vst1 = st + kPrefixStageBytes + kPrefixKBytes;
         const int t0 = 2 * j * 16;
         const int valid0 = max(0, min(16, vis_max - t0));
         const int valid1 = max(0, min(16, vis_max - t0 - 16));
         const int lim0 = min(valid0, max(lim_col - t0, 0));
         const int lim1 = min(valid1, max(lim_col - t0 - 16, 0));
         if (valid1 == 16 && min_lim - t0 >= 32)
-          tile_core2<false>(S, ka0, ka1, vr0, vr1, qb, 16, 16, lim0, lim1, q, p.scale_log2);
+          tile_core2<false>(S, ka0, ka1, vst0, vst1, vtr, qb, 16, 16, lim0, lim1, q, p.scale_log2);
         else
-          tile_core2<true>(S, ka0, ka1, vr0, vr1, qb, valid0, valid1, lim0, lim1, q, p.scale_log2);
+          tile_core2<true>(S, ka0, ka1, vst0, vst1, vtr, qb, valid0, valid1, lim0, lim1, q, p.scale_log2);
       }
     }
   }
 
-  // Normalise and write bf16: lane (q, n) holds O[rows 4q+r][dims 8n .. 8n+7].
+  // Normalise and write bf16: lane (q, n) holds O[rows 4q+r][dims 16j + n].
   const float lcol = group_sum4(S.l[0]);
   const float inv = lcol > 0.f ? 1.0f / lcol : 0.f;
 #pragma unroll
@@ -871,13 +878,9 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
     const int R = row0 + 4 * q + r;
     const float f = column_value(inv, q, r);
     if (R < rows) {
-      uint16_t* orow = p.out + ((size_t)(qs + R / G) * p.num_q_heads + g * G + R % G) * kD + 8 * n;
-      uint4 packed;
-      packed.x = bf16_rne(S.o[0][0][r] * f) | (bf16_rne(S.o[0][1][r] * f) << 16);
-      packed.y = bf16_rne(S.o[0][2][r] * f) | (bf16_rne(S.o[0][3][r] * f) << 16);
-      packed.z = bf16_rne(S.o[0][4][r] * f) | (bf16_rne(S.o[0][5][r] * f) << 16);
-      packed.w = bf16_rne(S.o[0][6][r] * f) | (bf16_rne(S.o[0][7][r] * f) << 16);
-      *reinterpret_cast<uint4*>(orow) = packed;
+      uint16_t* orow = p.out + ((size_t)(qs + R / G) * p.num_q_heads + g * G + R % G) * kD + n;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) orow[16 * j] = (uint16_t)bf16_rne(S.o[0][j][r] * f);
     }
   }
 }
