@@ -888,6 +888,8 @@ int pa_gather_tiles(const pa_kv_pool* pool, const int32_t* block_tables, int32_t
     return fail(PA_EINVAL, "%s: block_tables/spans/sink are not 4-byte aligned", fn);
   if (batch < 1 || bt_stride < 1)
     return fail(PA_EINVAL, "%s: batch %d and bt_stride %d must be >= 1", fn, batch, bt_stride);
+  if ((int64_t)bt_stride * PA_BLOCK_SIZE > 0x7fffffffLL)
+    return fail(PA_EINVAL, "%s: bt_stride %d: the table row spans more than 2^31 tokens", fn, bt_stride);
   if ((int64_t)num_spans * pool->num_kv_heads > 0x7fffffffLL)
     return fail(PA_EINVAL, "%s: %d spans x %d KV heads exceed the grid limit", fn, num_spans,
                 pool->num_kv_heads);

@@ -201,6 +201,7 @@ def test_gather_tiles_validation():
     cases = [(dict(num_spans=-1), "num_spans"), (dict(block_tables=0), "NULL"),
              (dict(spans=0), "NULL"), (dict(sink=0), "NULL"), (dict(spans=0x60002), "aligned"),
              (dict(batch=0), "batch"), (dict(bt_stride=0), "bt_stride"),
+             (dict(bt_stride=1 << 27), "2^31 tokens"),
              (dict(num_spans=1 << 28), "grid"), (dict(tiles_in_flight=3), "tiles_in_flight"),
              (dict(tiles_in_flight=0, num_spans=0), "tiles_in_flight")]
     for over, msg in cases:
