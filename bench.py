@@ -617,31 +617,55 @@ def main():
     # once), in the decode's grid shape, read with no arithmetic
     spans = base.tile_spans()
     n_spans = int(spans.shape[0])
-    spans_dev = torch.from_numpy(spans).to(dev)
     sink = torch.empty(max(1, n_spans * w.num_kv_heads * 4), dtype=torch.int32, device=dev)
-    gather_us = {}
-    for nif in (2, 4):
-        for i in range(3):
-            base.gather_tiles(spans_dev, n_spans, sink, sh, reps[i % R][0], nif)
-        torch.cuda.synchronize()
-        e_dec[0].record(stream)
-        for i in range(K):
-            base.gather_tiles(spans_dev, n_spans, sink, sh, reps[i % R][0], nif)
-        e_dec[1].record(stream)
-        torch.cuda.synchronize()
-        gather_us[nif] = 1e3 * e_dec[0].elapsed_time(e_dec[1]) / K
+
+    def time_gather(table, stride, rows, span_arr):
+        """us per call at ring depths 2 and 4, rotating the replicas like the decode."""
+        sd = torch.from_numpy(np.ascontiguousarray(span_arr, dtype=np.int32)).to(dev)
+        us = {}
+        for nif in (2, 4):
+            call = lambda i: binding.pa_gather_tiles(reps[i % R][0], table, stride, rows, sd,  # noqa: E731
+                                                     n_spans, sink, sh, nif)
+            for i in range(3):
+                call(i)
+            torch.cuda.synchronize()
+            e_dec[0].record(stream)
+            for i in range(K):
+                call(i)
+            e_dec[1].record(stream)
+            torch.cuda.synchronize()
+            us[nif] = 1e3 * e_dec[0].elapsed_time(e_dec[1]) / K
+        return us
+
+    gather_us = time_gather(base.bt, base.bt_stride, base.batch, spans)
     best_nif = min(gather_us, key=gather_us.get)
     gather_avg = gather_us[best_nif] / 1e3
-    tiles_read = int(sum((int(e) - (int(s) & ~15) + 15) // 16 for _, s, e in spans)) * w.num_kv_heads
+    span_blocks = [(int(e) - (int(s) & ~15) + 15) // 16 for _, s, e in spans]
+    tiles_read = int(sum(span_blocks)) * w.num_kv_heads
     gather_bytes = tiles_read * 2 * 16 * w.head_dim * 2
+    # the same spans with every span's blocks laid out contiguously (ids in
+    # order, one table row per span): the same bytes without fragmentation
+    crow = max(1, max(span_blocks, default=1))
+    ctab = np.zeros((max(1, n_spans), crow), dtype=np.int32)
+    nxt = 0
+    for i, nb in enumerate(span_blocks):
+        ctab[i, :nb] = np.arange(nxt, nxt + nb) % w.num_blocks
+        nxt += nb
+    cspans = np.stack([np.arange(n_spans), np.zeros(n_spans, np.int64),
+                       16 * np.asarray(span_blocks, np.int64)], axis=1) if n_spans else spans
+    contig_us = time_gather(torch.from_numpy(ctab).to(dev), crow, max(1, n_spans), cspans)
+    contig_avg = min(contig_us.values()) / 1e3
     gather_line = {"us_per_call": round(gather_avg * 1e3, 3), "kv_bytes": gather_bytes,
                    "tiles_in_flight": best_nif,
                    "us_by_tiles_in_flight": {str(k): round(v, 3) for k, v in gather_us.items()},
                    "gbps": round(gather_bytes / (gather_avg * 1e-3) / 1e9, 1),
                    "spans": n_spans,
                    "decode_time_over_gather": round(dec_avg / gather_avg, 3),
+                   "contiguous_us_per_call": round(contig_avg * 1e3, 3),
+                   "contiguous_gbps": round(gather_bytes / (contig_avg * 1e-3) / 1e9, 1),
                    "note": "pa_gather_tiles: the K/V tiles of this step (each once) read in the "
-                           "decode's grid shape with no arithmetic (the faster ring depth)"}
+                           "decode's grid shape with no arithmetic (the faster ring depth); "
+                           "contiguous: the same spans with each span's blocks stored in order"}
     log(f"gather reference: {gather_line}")
 
     # hot: one replica, same loop (optional)
