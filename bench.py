@@ -111,7 +111,19 @@ def _oracle_chunk(seqs):
     return len(seqs)
 
 
-def cpu_baseline(w, alg_bytes, min_seconds=10.0):
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(w, alg_bytes, min_seconds=10.0, logical_bytes=None):
     """Time the CPU oracle on whole decode steps of the same batch.
 
     The oracle runs over the batch's sequences in a process pool (one BLAS
@@ -139,7 +151,10 @@ def cpu_baseline(w, alg_bytes, min_seconds=10.0):
             "kind": "oracle", "sample": f"{steps} full decode steps of the same batch "
             f"({w.batch} sequences) in {el:.1f} s; fp64 numpy oracle, process pool, "
             f"1 BLAS thread per worker", "seconds_per_step": round(sec_per_step, 4),
-            "decode_steps_per_s": round(1.0 / sec_per_step, 3)}
+            "decode_steps_per_s": round(1.0 / sec_per_step, 3),
+            "logical_kv_gbps": (round(logical_bytes / sec_per_step / 1e9, 4)
+                                if logical_bytes else None),
+            "cpu_model": _cpu_model(), "numpy": np.__version__}
 
 
 # ------------------------------------------------------------------ traffic
@@ -456,7 +471,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline and not args.profile_loop:
         log("cpu baseline (oracle) ...")
-        cpu = cpu_baseline(w, alg_bytes, args.cpu_seconds)
+        cpu = cpu_baseline(w, alg_bytes, args.cpu_seconds, logical_bytes)
         log(f"cpu baseline: {cpu}")
 
     import torch
