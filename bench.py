@@ -408,7 +408,8 @@ def main():
     ap.add_argument("--replicas", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--hot", action="store_true", help="also time steps on a single replica")
+    ap.add_argument("--hot", action=argparse.BooleanOptionalAction, default=True,
+                    help="also time steps on a single replica (cache-warm); --no-hot skips it")
     ap.add_argument("--cascade", choices=["auto", "on", "off"], default="auto",
                     help="shared-prefix cascade (auto: on when the batch shares a prefix)")
     ap.add_argument("--prefix-partition-size", type=int, default=None,
