@@ -512,6 +512,10 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
 // lse = -inf when it attended to nothing.
 constexpr int kPrefixRowsPerWg = 16 * kWaves;
 constexpr int kPrefixRing = 4;                  // blocks whose quarter is in flight per wavefront (even)
+// The pair loops publish ring slots 2h, 2h+1 and only then refill them, so
+// the first kRing - 2 blocks must be loaded before the loop: at least two
+// pairs of slots.
+static_assert(kPrefixRing >= 4 && kPrefixRing % 2 == 0, "the prefix ring needs two pairs of slots");
 constexpr int kPrefixKBytes = 16 * kKPitch;     // staged K tile (swizzled, k_stage)
 constexpr int kPrefixStageBytes = kPrefixKBytes + 16 * kD * 2;  // + V tile, row pitch 256
 constexpr int kPrefixLdsBytes = 4 * kPrefixStageBytes;   // two stages of a block pair
@@ -734,6 +738,7 @@ __device__ __forceinline__ void group_mfma_body(const PrefixParams& p, int wg_in
 // normalises its rows and writes them as bf16.
 constexpr int kExtendRowsPerWg = 16 * kWaves;
 constexpr int kExtendRing = 6;                  // blocks whose quarter is in flight per wavefront (even)
+static_assert(kExtendRing >= 4 && kExtendRing % 2 == 0, "the extend ring needs two pairs of slots");
 constexpr int kExtendIdOffset = 4 * kPrefixStageBytes;   // after two stages of a block pair
 constexpr int kExtendLdsBytes = kExtendIdOffset + kExtendMaxTokens / 16 * 4;   // + the block ids
 
