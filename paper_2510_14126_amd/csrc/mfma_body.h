@@ -303,13 +303,20 @@ __device__ __forceinline__ int k_arow(int n) { return 4 * (n & 3) + (n >> 2); }
 // touch 16 distinct positions per instruction, with no padding.
 __device__ __forceinline__ int k_stage(int r, int c) { return r * kKPitch + ((c ^ k_arow(r)) << 4); }
 
+// Window position of row r in a staged V tile: v_swz(r) = (r ^ r/4) & 7.
+// A transposing read of one window serves each group of 16 lanes from rows
+// q, q+4, q+8, q+12, and v_swz puts those four rows at window positions
+// that differ modulo 4, i.e. on four different sets of eight banks (a 32-byte
+// window covers 8 of the 32 four-byte banks, and windows w and w+4 share
+// them): each group's read is free of bank conflicts.
+__device__ __forceinline__ int v_swz(int r) { return (r ^ (r >> 2)) & 7; }
+
 // LDS byte offset of 16-byte chunk c (dims 8c .. 8c+7) of token row r in a
 // staged V tile: rows of 256 bytes, each of eight 32-byte windows (dims
-// 16w .. 16w+15) at window position w ^ (r & 7).  Writers (16 lanes per row)
-// fill whole rows; the transposing reads of tile_core2 (16 rows x one window
-// per instruction) then spread over all eight window positions.
+// 16w .. 16w+15) at window position w ^ v_swz(r).  Writers (16 lanes per
+// row) fill whole rows.
 __device__ __forceinline__ int v_stage(int r, int c) {
-  return r * 256 + ((((c >> 1) ^ (r & 7)) << 5) | ((c & 1) << 4));
+  return r * 256 + ((((c >> 1) ^ v_swz(r)) << 5) | ((c & 1) << 4));
 }
 
 // Lane (q, n)'s address in a staged V tile for the transposing read of
@@ -318,7 +325,7 @@ __device__ __forceinline__ int v_stage(int r, int c) {
 // 4k + n/4 of its group, i.e. V[token q + 4k][dim 16j + n] for k = 0..3.
 __device__ __forceinline__ int v_tr(int q, int n) {
   const int r = q + 4 * (n >> 2);
-  return r * 256 + ((r & 7) << 5) + ((n & 3) << 3);
+  return r * 256 + (v_swz(r) << 5) + ((n & 3) << 3);
 }
 
 // One block of a per-sequence work item: the wavefront's own K tile goes

@@ -23,13 +23,30 @@ def k_stage(r, c):
     return r * 256 + ((c ^ k_arow(r)) << 4)
 
 
+def v_swz(r):
+    return (r ^ (r >> 2)) & 7
+
+
 def v_stage(r, c):
-    return r * 256 + ((((c >> 1) ^ (r & 7)) << 5) | ((c & 1) << 4))
+    return r * 256 + ((((c >> 1) ^ v_swz(r)) << 5) | ((c & 1) << 4))
 
 
 def v_tr(q, n):
     r = q + 4 * (n >> 2)
-    return r * 256 + ((r & 7) << 5) + ((n & 3) << 3)
+    return r * 256 + (v_swz(r) << 5) + ((n & 3) << 3)
+
+
+def bank_conflict_degree(addrs, width, lanes):
+    """Worst number of distinct 4-byte words per bank (32 banks) over groups of
+    `lanes` consecutive lanes, each lane accessing `width` bytes."""
+    worst = 0
+    for g in range(0, len(addrs), lanes):
+        words = {}
+        for a in addrs[g:g + lanes]:
+            for w in range(width // 4):
+                words.setdefault((a // 4 + w) % 32, set()).add(a // 4 + w)
+        worst = max(worst, max(len(v) for v in words.values()))
+    return worst
 
 
 def stage(tile, place):
@@ -67,11 +84,22 @@ def test_v_tr_reads_give_the_pv_b_operand():
             assert list(got[lane]) == [v[q + 4 * k, 16 * j + n] for k in range(4)]
 
 
-def test_v_tr_spreads_each_read_over_all_windows():
-    """Each 16-row read of one window touches all eight window positions twice."""
+def test_v_tr_reads_are_free_of_bank_conflicts():
+    """Each 16-lane group of a transposing read reaches 32 distinct banks
+    (the former window position r & 7 put a group's four rows on the same
+    eight banks: 4-way conflicts)."""
     for j in range(8):
-        windows = [((v_tr(lane >> 4, lane & 15) ^ (j << 5)) >> 5) & 7 for lane in range(0, 64, 4)]
-        assert sorted(windows) == sorted(list(range(8)) * 2)
+        addrs = [v_tr(lane >> 4, lane & 15) ^ (j << 5) for lane in range(64)]
+        assert bank_conflict_degree(addrs, 8, 16) == 1
+    old = [(q + 4 * (n >> 2)) * 256 + (((q + 4 * (n >> 2)) & 7) << 5) + ((n & 3) << 3)
+           for q in range(4) for n in range(16)]
+    assert bank_conflict_degree(old, 8, 16) == 4
+
+
+def test_k_reads_are_free_of_bank_conflicts_per_8_lanes():
+    for s in range(4):
+        addrs = [k_stage(k_arow(lane & 15), 4 * s + (lane >> 4)) for lane in range(64)]
+        assert bank_conflict_degree(addrs, 16, 8) == 1
 
 
 def test_k_stage_gives_the_a_operand_without_conflicts():
