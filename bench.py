@@ -220,6 +220,54 @@ def ingest_counters(fetch_csv, write_csv, workload_name, kernel_prefix, command_
     print(out)
 
 
+def ingest_sq(csv_paths, workload_name, kernel_substr, command_note, stem):
+    """Write a per-dispatch summary of SQ (shader sequencer) counters for one kernel."""
+    import csv
+    import collections
+    m, n = {}, 0
+    name = None
+    for path in csv_paths:
+        per = collections.defaultdict(lambda: collections.defaultdict(list))
+        for r in csv.DictReader(open(path)):
+            per[r["Kernel_Name"]][r["Counter_Name"]].append(float(r["Counter_Value"]))
+        ks = [k for k in per if kernel_substr in k]
+        if not ks:
+            raise SystemExit(f"no {kernel_substr} dispatches in {path}")
+        name = ks[0]
+        for c, v in per[name].items():
+            m[c] = sum(v) / len(v)
+            n = len(v)
+    simds = 1024                      # 256 CUs x 4 SIMDs
+    xcds = 8
+    lines = []
+    if "GRBM_GUI_ACTIVE" in m and "SQ_VALU_MFMA_BUSY_CYCLES" in m:
+        gpu_cycles = m["GRBM_GUI_ACTIVE"] / xcds
+        lines.append(f"| matrix-core busy (SQ_VALU_MFMA_BUSY_CYCLES / (SIMDs x GRBM_GUI_ACTIVE per XCD)) | "
+                     f"{100 * m['SQ_VALU_MFMA_BUSY_CYCLES'] / (simds * gpu_cycles):.1f}% |")
+    if "SQ_WAVE_CYCLES" in m:
+        for c, label in (("SQ_WAIT_INST_ANY", "wave cycles waiting on an instruction dependency"),
+                         ("SQ_WAIT_INST_LDS", "wave cycles waiting on LDS"),
+                         ("SQ_ACTIVE_INST_VALU", "wave cycles issuing VALU"),
+                         ("SQ_ACTIVE_INST_LDS", "wave cycles issuing LDS")):
+            if c in m:
+                lines.append(f"| {label} ({c} / SQ_WAVE_CYCLES) | {100 * m[c] / m['SQ_WAVE_CYCLES']:.1f}% |")
+    if "SQ_LDS_BANK_CONFLICT" in m and "SQ_LDS_IDX_ACTIVE" in m:
+        lines.append(f"| LDS bank-conflict cycles / LDS active cycles | "
+                     f"{100 * m['SQ_LDS_BANK_CONFLICT'] / max(1.0, m['SQ_LDS_IDX_ACTIVE']):.1f}% |")
+    if "SQ_INSTS_VALU" in m and "SQ_INSTS_MFMA" in m and m["SQ_INSTS_MFMA"] > 0:
+        lines.append(f"| VALU instructions per MFMA | {m['SQ_INSTS_VALU'] / m['SQ_INSTS_MFMA']:.2f} |")
+    out = os.path.join(PROFILE_DIR, f"{stem}.md")
+    with open(out, "w") as fh:
+        fh.write(f"# SQ counters: {name} on the {workload_name} workload\n\n"
+                 f"Commands (run from /tmp with TMPDIR=/tmp):\n\n{command_note}\n\n"
+                 f"Per-dispatch means over {n} dispatches (whole GPU).\n\n"
+                 "| counter | per dispatch |\n|---|---|\n")
+        for c in sorted(m):
+            fh.write(f"| {c} | {m[c]:,.0f} |\n")
+        fh.write("\n| derived | value |\n|---|---|\n" + "\n".join(lines) + "\n")
+    print(out)
+
+
 def ingest_stats(stats_csv, workload_name, command_note, stem=None):
     """Write the kernel-duration summary from a rocprofv3 --stats kernel_stats.csv."""
     import csv
@@ -423,6 +471,9 @@ def main():
                     help="replay each step from a captured HIP graph (one per replica)")
     ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--ingest-stats", metavar="KERNEL_STATS_CSV")
+    ap.add_argument("--ingest-sq", nargs="+", metavar="COUNTER_CSV",
+                    help="write an SQ-counter summary (with --sq-kernel and --profile-name)")
+    ap.add_argument("--sq-kernel", default="cascade_kernel")
     ap.add_argument("--command-note", default="")
     ap.add_argument("--extend", action="store_true",
                     help="also time extend (chunked prefill) attention: each sequence's tokens after "
@@ -438,6 +489,11 @@ def main():
                          "for hardware-counter runs")
     args = ap.parse_args()
 
+    if args.ingest_sq:
+        from workloads import CONFIG_NAMES
+        ingest_sq(args.ingest_sq, CONFIG_NAMES[args.config], args.sq_kernel, args.command_note,
+                  args.profile_name or f"sq_{CONFIG_NAMES[args.config]}")
+        return
     if args.ingest_counters or args.ingest_stats:
         from workloads import CONFIG_NAMES
         name = CONFIG_NAMES[args.config]
