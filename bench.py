@@ -740,18 +740,23 @@ def main():
                            "contiguous: the same spans with each span's blocks stored in order"}
     log(f"gather reference: {gather_line}")
 
-    # hot: one replica, same loop (optional)
-    hot = []
-    for i in range(K if args.hot else 0):
-        e0 = torch.cuda.Event(enable_timing=True); e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
+    # hot: K steps back to back on one replica (its working set stays in the
+    # caches), timed like the main loop
+    hot_ms = None
+    if args.hot:
         decode(0)
         if split:
             reduce()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True); e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(K):
+            decode(0)
+            if split:
+                reduce()
         e1.record(stream)
-        hot.append((e0, e1))
-    torch.cuda.synchronize()
-    hot_ms = float(np.mean([a.elapsed_time(b) for a, b in hot])) if hot else None
+        torch.cuda.synchronize()
+        hot_ms = e0.elapsed_time(e1) / K
 
     # KV append of the step's new token, timed the same way.  The rows written
     # are the ones already stored at slot ctx-1, so the pools stay unchanged
