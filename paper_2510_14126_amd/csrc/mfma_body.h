@@ -199,100 +199,6 @@ __device__ __forceinline__ void tile_core(MfmaState<NT>& S, const u32x4_t (&ka)[
   }
 }
 
-// Two 16-token blocks at once against one column tile.  Lane (q, n) holds
-// the scores of tokens 4r+q (r = 0..3) of both blocks for column n, so with
-// the contraction index k = 8q + e standing for token 4e+q of block 0
-// (e < 4) and token 4(e-4)+q of block 1 (e >= 4), the eight probabilities
-// are exactly the A operand of one v_mfma_f32_16x16x32_bf16 per 16 output
-// dims: PV runs at the full bf16 rate and the softmax bookkeeping happens
-// once per 32 tokens.  The B operand of instruction j (output column n =
-// dim 16j + n) comes straight from the staged V tiles (vst0, vst1; layout
-// v_stage) by two transposing LDS reads, one per block; vtr is the lane's
-// v_tr offset.  valid0/valid1 and lim0/lim1 as `valid` and `limit` of
-// tile_core, per block (a block with valid = 0 contributes nothing).
-template <bool TAIL>
-__device__ __forceinline__ void tile_core2(MfmaState<1>& S, const u32x4_t (&ka0)[4],
-                                           const u32x4_t (&ka1)[4], const lds_u8_t* vst0,
-                                           const lds_u8_t* vst1, int vtr, const uint4 (&qb)[1][4],
-                                           int valid0, int valid1, int lim0, int lim1, int q,
-                                           float scale_log2) {
-  const floatx4_t z = {0.f, 0.f, 0.f, 0.f};
-  floatx4_t a0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-      __builtin_bit_cast(bf16x8_t, ka0[0]), __builtin_bit_cast(bf16x8_t, qb[0][0]), z, 0, 0, 0);
-  floatx4_t a1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-      __builtin_bit_cast(bf16x8_t, ka1[0]), __builtin_bit_cast(bf16x8_t, qb[0][0]), z, 0, 0, 0);
-#pragma unroll
-  for (int s = 1; s < 4; ++s) {
-    a0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka0[s]),
-                                                 __builtin_bit_cast(bf16x8_t, qb[0][s]), a0, 0, 0, 0);
-    a1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka1[s]),
-                                                 __builtin_bit_cast(bf16x8_t, qb[0][s]), a1, 0, 0, 0);
-  }
-
-  float sc[8];
-  bool raise = false;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int r = e & 3;
-    float x = (e < 4 ? a0[r] : a1[r]) * scale_log2;
-    if (TAIL && 4 * r + q >= (e < 4 ? lim0 : lim1)) x = -__builtin_inff();
-    sc[e] = x;
-    raise |= x > S.m[0] + kLazyRescale;
-  }
-  if (__builtin_amdgcn_ballot_w64(raise) != 0) {
-    float b = sc[0];
-#pragma unroll
-    for (int e = 1; e < 8; ++e) b = fmaxf(b, sc[e]);
-    const float bm = group_max4(b);
-    const float mn = bm > S.m[0] + kLazyRescale ? bm : S.m[0];
-    const float alpha = mn == -__builtin_inff() ? 1.f : fast_exp2(S.m[0] - mn);
-    S.l[0] *= alpha;
-    S.m[0] = mn;
-    float ar[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) ar[r] = column_value(alpha, q, r);
-#pragma unroll
-    for (int blk = 0; blk < 8; ++blk)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) S.o[0][blk][r] *= ar[r];
-  }
-
-  const float mref = S.m[0] == -__builtin_inff() ? 0.f : S.m[0];
-  // Probabilities rounded to bf16 (the A operand); the column sum uses the
-  // same rounded values, from the packed words by v_dot2 against (1, 1).
-  bf16x8_t pa;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) pa[e] = (__bf16)fast_exp2(sc[e] - mref);
-  {
-    const u32x4_t pw = __builtin_bit_cast(u32x4_t, pa);
-    float lsum = dot2_bf16(pw[0], 0x3F803F80u, 0.f);
-    lsum = dot2_bf16(pw[1], 0x3F803F80u, lsum);
-    lsum = dot2_bf16(pw[2], 0x3F803F80u, lsum);
-    S.l[0] += dot2_bf16(pw[3], 0x3F803F80u, lsum);
-  }
-
-  // Element e of a block's B words is its token 4e + q; rows past `valid`
-  // are zeroed (their V may be anything, NaN included).
-  uint32_t m0 = 0xffffffffu, m1 = 0xffffffffu, m2 = 0xffffffffu, m3 = 0xffffffffu;
-  if constexpr (TAIL) {
-    m0 = (q < valid0 ? 0xffffu : 0u) | (q + 4 < valid0 ? 0xffff0000u : 0u);
-    m1 = (q + 8 < valid0 ? 0xffffu : 0u) | (q + 12 < valid0 ? 0xffff0000u : 0u);
-    m2 = (q < valid1 ? 0xffffu : 0u) | (q + 4 < valid1 ? 0xffff0000u : 0u);
-    m3 = (q + 8 < valid1 ? 0xffffu : 0u) | (q + 12 < valid1 ? 0xffff0000u : 0u);
-  }
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int off = vtr ^ (j << 5);
-    const uint2 b0 = __builtin_bit_cast(
-        uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vst0 + off)));
-    const uint2 b1 = __builtin_bit_cast(
-        uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vst1 + off)));
-    const u32x4_t vb = {b0.x & m0, b0.y & m1, b1.x & m2, b1.y & m3};
-    S.o[0][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, __builtin_bit_cast(bf16x8_t, vb), S.o[0][j],
-                                                        0, 0, 0);
-  }
-}
-
 // Row of the K tile that lane (q, n) supplies as A row n: token 4(n%4) + n/4.
 __device__ __forceinline__ int k_arow(int n) { return 4 * (n & 3) + (n >> 2); }
 
@@ -327,6 +233,144 @@ __device__ __forceinline__ int v_tr(int q, int n) {
   const int r = q + 4 * (n >> 2);
   return r * 256 + (v_swz(r) << 5) + ((n & 3) << 3);
 }
+
+// One staged block in the shared-span pass and extend: its K tile (k_stage
+// layout) then its V tile (v_stage layout).
+constexpr int kPrefixKBytes = 16 * kKPitch;
+constexpr int kPrefixStageBytes = kPrefixKBytes + 16 * kD * 2;
+// The shared-prefix pass streams its blocks in pairs (one LDS stage and one
+// barrier per pair) through a ring of kPrefixRing quarter-blocks: the first
+// pair is loaded before the loop and each pair's successor while it is
+// published.  Extend streams kExtendStageBlocks blocks per stage through
+// kExtendRingSets sets of slots, each stage loaded kExtendLoadAhead stages
+// before it is published (1 <= AHEAD <= SETS; stage j in set j % SETS).
+// Measured fastest: the prefix pass as described (the generic loop at the
+// same depth was 4% slower on the generator batch), extend at (2, 2, 2),
+// where it needs 162 VGPRs and runs three wavefronts per SIMD.
+constexpr int kPrefixStageBlocks = 2;
+constexpr int kPrefixRing = 4;
+constexpr int kExtendStageBlocks = 2;
+constexpr int kExtendRingSets = 2;
+constexpr int kExtendLoadAhead = 2;
+static_assert(kPrefixRing == 2 * kPrefixStageBlocks, "two pairs of slots");
+static_assert(kExtendStageBlocks % 2 == 0, "blocks go in pairs");
+static_assert(1 <= kExtendLoadAhead && kExtendLoadAhead <= kExtendRingSets, "loads stay in the ring");
+
+// NB 16-token blocks (NB even) staged at st + b * kPrefixStageBytes (K in the
+// k_stage layout, V in the v_stage layout) against one column tile.  The
+// QK^T of every block comes first (independent MFMA chains); lane (q, n)
+// then holds the scores of tokens 4r+q of each block for column n, and one
+// online-softmax step covers all NB*16 tokens.  For PV, blocks 2p and 2p+1
+// form the contraction index k = 8q + e (token 4e+q of block 2p for e < 4,
+// token 4(e-4)+q of block 2p+1 for e >= 4), so the lane's eight
+// probabilities are exactly the A operand of one v_mfma_f32_16x16x32_bf16
+// per 16 output dims (output column n = dim 16j + n), whose B operand two
+// transposing LDS reads deliver straight from the staged V tiles (vtr is
+// the lane's v_tr offset).  valid[b]: rows of block b that hold tokens of the
+// span (0: an empty block); lim[b]: rows of block b this lane's column may
+// see.  Rows past valid[b] are zeroed in the B operand (their V may be
+// anything, NaN included).
+template <bool TAIL, int NB>
+__device__ __forceinline__ void tile_core_nb(MfmaState<1>& S, const lds_u8_t* st, int vtr,
+                                             const uint4 (&qb)[1][4], const int (&valid)[NB],
+                                             const int (&lim)[NB], int q, int n, float scale_log2) {
+  static_assert(NB % 2 == 0, "blocks go in pairs through the PV contraction");
+  const floatx4_t z = {0.f, 0.f, 0.f, 0.f};
+  // K operands of every block first, then the score MFMAs interleaved over
+  // the blocks so that consecutive MFMAs do not depend on each other.
+  u32x4_t ka[NB][4];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      ka[b][c] = *reinterpret_cast<const lds_u32x4_t*>(st + b * kPrefixStageBytes + k_stage(k_arow(n), 4 * c + q));
+  floatx4_t a[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+    a[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[b][0]),
+                                                   __builtin_bit_cast(bf16x8_t, qb[0][0]), z, 0, 0, 0);
+#pragma unroll
+  for (int c = 1; c < 4; ++c)
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+      a[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[b][c]),
+                                                     __builtin_bit_cast(bf16x8_t, qb[0][c]), a[b], 0, 0, 0);
+
+  float sc[4 * NB];
+  bool raise = false;
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float x = a[b][r] * scale_log2;
+      if (TAIL && 4 * r + q >= lim[b]) x = -__builtin_inff();
+      sc[4 * b + r] = x;
+      raise |= x > S.m[0] + kLazyRescale;
+    }
+  if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+    float bmax = sc[0];
+#pragma unroll
+    for (int e = 1; e < 4 * NB; ++e) bmax = fmaxf(bmax, sc[e]);
+    const float bm = group_max4(bmax);
+    const float mn = bm > S.m[0] + kLazyRescale ? bm : S.m[0];
+    const float alpha = mn == -__builtin_inff() ? 1.f : fast_exp2(S.m[0] - mn);
+    S.l[0] *= alpha;
+    S.m[0] = mn;
+    float ar[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) ar[r] = column_value(alpha, q, r);
+#pragma unroll
+    for (int blk = 0; blk < 8; ++blk)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) S.o[0][blk][r] *= ar[r];
+  }
+
+  const float mref = S.m[0] == -__builtin_inff() ? 0.f : S.m[0];
+  // Probabilities rounded to bf16 (the A operands: element e of pa[p] is
+  // sc[8p + e]); the column sum uses the same rounded values, from the
+  // packed words by v_dot2 against (1, 1).
+  bf16x8_t pa[NB / 2];
+  float lsum = 0.f;
+#pragma unroll
+  for (int pp = 0; pp < NB / 2; ++pp) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pa[pp][e] = (__bf16)fast_exp2(sc[8 * pp + e] - mref);
+    const u32x4_t pw = __builtin_bit_cast(u32x4_t, pa[pp]);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) lsum = dot2_bf16(pw[w], 0x3F803F80u, lsum);
+  }
+  S.l[0] += lsum;
+
+  // Element e of a block's B words is its token 4e + q.
+  uint32_t mlo[NB], mhi[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    mlo[b] = 0xffffffffu;
+    mhi[b] = 0xffffffffu;
+    if constexpr (TAIL) {
+      mlo[b] = (q < valid[b] ? 0xffffu : 0u) | (q + 4 < valid[b] ? 0xffff0000u : 0u);
+      mhi[b] = (q + 8 < valid[b] ? 0xffffu : 0u) | (q + 12 < valid[b] ? 0xffff0000u : 0u);
+    }
+  }
+#pragma unroll
+  for (int pp = 0; pp < NB / 2; ++pp) {
+    const lds_u8_t* v0 = st + (2 * pp) * kPrefixStageBytes + kPrefixKBytes;
+    const lds_u8_t* v1 = v0 + kPrefixStageBytes;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int off = vtr ^ (j << 5);
+      const uint2 b0 = __builtin_bit_cast(
+          uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(v0 + off)));
+      const uint2 b1 = __builtin_bit_cast(
+          uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(v1 + off)));
+      const u32x4_t vb = {b0.x & mlo[2 * pp], b0.y & mhi[2 * pp], b1.x & mlo[2 * pp + 1],
+                          b1.y & mhi[2 * pp + 1]};
+      S.o[0][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[pp], __builtin_bit_cast(bf16x8_t, vb),
+                                                          S.o[0][j], 0, 0, 0);
+    }
+  }
+}
+
 
 // One block of a per-sequence work item: the wavefront's own K tile goes
 // through `stage` (kStageBytes of its LDS) to reach the A-operand layout;
@@ -518,14 +562,7 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
 // afterwards.  Every row writes its (o, lse) partial for the partition,
 // lse = -inf when it attended to nothing.
 constexpr int kPrefixRowsPerWg = 16 * kWaves;
-constexpr int kPrefixRing = 4;                  // blocks whose quarter is in flight per wavefront (even)
-// The pair loops publish ring slots 2h, 2h+1 and only then refill them, so
-// the first kRing - 2 blocks must be loaded before the loop: at least two
-// pairs of slots.
-static_assert(kPrefixRing >= 4 && kPrefixRing % 2 == 0, "the prefix ring needs two pairs of slots");
-constexpr int kPrefixKBytes = 16 * kKPitch;     // staged K tile (swizzled, k_stage)
-constexpr int kPrefixStageBytes = kPrefixKBytes + 16 * kD * 2;  // + V tile, row pitch 256
-constexpr int kPrefixLdsBytes = 4 * kPrefixStageBytes;   // two stages of a block pair
+constexpr int kPrefixLdsBytes = 2 * kPrefixStageBlocks * kPrefixStageBytes;   // two stages
 
 // Rows and tokens of one shared-span workgroup: rows R = row0 .. (16 per
 // wavefront) of span rows 0 .. total_rows-1, row R being sequence seq0 + R / G
@@ -606,10 +643,12 @@ __device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, c
     dst[1] = make_uint4(v[0], v[1], v[2], v[3]);
   };
 
-  // Blocks go in pairs through tile_core2: both quarters of a pair are
-  // published to one LDS stage (double-buffered), one barrier per pair.  The
-  // two blocks of a pair need not be adjacent; an odd last block pairs with an
-  // empty one (valid = 0: fully masked).
+  // The blocks go in pairs: every wavefront publishes its quarter of both
+  // blocks of pair j to one LDS stage (double-buffered), loads the quarters
+  // of pair j+1 into the other two ring slots, one barrier, then every
+  // wavefront runs its tile against the pair.  The two blocks of a pair need
+  // not be adjacent; an odd last block pairs with an empty one (valid = 0).
+  constexpr int NB = 2;
   constexpr int kRing = kPrefixRing;
   uint4 ring[kRing][2];
 #pragma unroll
@@ -633,26 +672,21 @@ __device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, c
         load(ring[(2 * h + kRing - 2) % kRing], 2 * j + kRing - 2);
         load(ring[(2 * h + kRing - 1) % kRing], 2 * j + kRing - 1);
         __syncthreads();
-
-        u32x4_t ka0[4], ka1[4];
+        int valid[NB], lim[NB];
+        bool fast = true;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          ka0[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_stage(k_arow(n), 4 * c + q));
-          ka1[c] = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + k_stage(k_arow(n), 4 * c + q));
+        for (int s = 0; s < NB; ++s) {
+          const int i = NB * j + s;
+          const bool has = i < nblk;
+          const int tb = has ? start + block_of(i) * 16 : end;
+          valid[s] = has ? min(16, end - tb) : 0;
+          lim[s] = min(valid[s], max(ctx - tb, 0));
+          fast = fast && valid[s] == 16 && min_ctx - tb >= 16;
         }
-        const lds_u8_t* vst0 = st + kPrefixKBytes;
-        const lds_u8_t* vst1 = st + kPrefixStageBytes + kPrefixKBytes;
-        const bool has1 = 2 * j + 1 < nblk;
-        const int ta = start + block_of(2 * j) * 16;
-        const int tb = has1 ? start + block_of(2 * j + 1) * 16 : end;
-        const int valid0 = min(16, end - ta);
-        const int valid1 = has1 ? min(16, end - tb) : 0;
-        const int lim0 = min(valid0, max(ctx - ta, 0));
-        const int lim1 = min(valid1, max(ctx - tb, 0));
-        if (valid0 == 16 && valid1 == 16 && min_ctx - ta >= 16 && min_ctx - tb >= 16)
-          tile_core2<false>(S, ka0, ka1, vst0, vst1, vtr, qb, 16, 16, lim0, lim1, q, p.scale_log2);
+        if (fast)
+          tile_core_nb<false, NB>(S, st, vtr, qb, valid, lim, q, n, p.scale_log2);
         else
-          tile_core2<true>(S, ka0, ka1, vst0, vst1, vtr, qb, valid0, valid1, lim0, lim1, q, p.scale_log2);
+          tile_core_nb<true, NB>(S, st, vtr, qb, valid, lim, q, n, p.scale_log2);
       }
     }
   }
@@ -744,9 +778,7 @@ __device__ __forceinline__ void group_mfma_body(const PrefixParams& p, int wg_in
 // stream stops at the workgroup's last visible token.  Each wavefront
 // normalises its rows and writes them as bf16.
 constexpr int kExtendRowsPerWg = 16 * kWaves;
-constexpr int kExtendRing = 6;                  // blocks whose quarter is in flight per wavefront (even)
-static_assert(kExtendRing >= 4 && kExtendRing % 2 == 0, "the extend ring needs two pairs of slots");
-constexpr int kExtendIdOffset = 4 * kPrefixStageBytes;   // after two stages of a block pair
+constexpr int kExtendIdOffset = 2 * kExtendStageBlocks * kPrefixStageBytes;   // after two stages
 constexpr int kExtendLdsBytes = kExtendIdOffset + kExtendMaxTokens / 16 * 4;   // + the block ids
 
 template <int G>
@@ -834,52 +866,51 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
     dst[1] = make_uint4(v[0], v[1], v[2], v[3]);
   };
 
-  // Blocks go in pairs: both quarters of a pair are published to one LDS
-  // stage (double-buffered), one barrier, then the two-block core.  An odd
-  // last block pairs with an empty one (valid = 0: fully masked).
-  constexpr int kRing = kExtendRing;
-  uint4 ring[kRing][2];
+  // The blocks go NB at a time: every wavefront publishes its quarter of
+  // each block of stage j to one LDS stage (double-buffered), loads the
+  // quarters of stage j + AHEAD, one barrier, then every wavefront runs its
+  // tiles against the stage.  Blocks past the stream are empty (valid = 0).
+  constexpr int NB = kExtendStageBlocks;
+  constexpr int SETS = kExtendRingSets;
+  constexpr int AHEAD = kExtendLoadAhead;
+  uint4 ring[SETS * NB][2];                     // stage j's blocks in slot set j % SETS
 #pragma unroll
-  for (int s = 0; s < kRing - 2; ++s) load(ring[s], s);
-  const int npair = (nblk + 1) >> 1;
-  for (int j0 = 0; j0 < npair; j0 += kRing / 2) {
+  for (int s = 0; s < AHEAD * NB; ++s) load(ring[s], s);
+  const int nit = (nblk + NB - 1) / NB;
+  for (int j0 = 0; j0 < nit; j0 += SETS) {
 #pragma unroll
-    for (int h = 0; h < kRing / 2; ++h) {
-      const int j = j0 + h;
-      if (j < npair) {                         // uniform over the workgroup
-        lds_u8_t* st = smem + (j & 1) * 2 * kPrefixStageBytes;
+  for (int h = 0; h < SETS; ++h) {
+    const int j = j0 + h;
+    if (j < nit) {                              // uniform over the workgroup
+      lds_u8_t* st = smem + (j & 1) * NB * kPrefixStageBytes;
 #pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          lds_u8_t* sb = st + e * kPrefixStageBytes;
-          const int s = 2 * h + e;
-          *reinterpret_cast<lds_u32x4_t*>(sb + k_stage(4 * wave + q, n)) =
-              u32x4_t{ring[s][0].x, ring[s][0].y, ring[s][0].z, ring[s][0].w};
-          *reinterpret_cast<lds_u32x4_t*>(sb + kPrefixKBytes + v_stage(4 * wave + q, n)) =
-              u32x4_t{ring[s][1].x, ring[s][1].y, ring[s][1].z, ring[s][1].w};
-        }
-        load(ring[(2 * h + kRing - 2) % kRing], 2 * j + kRing - 2);
-        load(ring[(2 * h + kRing - 1) % kRing], 2 * j + kRing - 1);
-        __syncthreads();
-
-        u32x4_t ka0[4], ka1[4];
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          ka0[c] = *reinterpret_cast<const lds_u32x4_t*>(st + k_stage(k_arow(n), 4 * c + q));
-          ka1[c] = *reinterpret_cast<const lds_u32x4_t*>(st + kPrefixStageBytes + k_stage(k_arow(n), 4 * c + q));
-        }
-        const lds_u8_t* vst0 = st + kPrefixKBytes;
-        const lds_u8_t* vst1 = st + kPrefixStageBytes + kPrefixKBytes;
-        const int t0 = 2 * j * 16;
-        const int valid0 = max(0, min(16, vis_max - t0));
-        const int valid1 = max(0, min(16, vis_max - t0 - 16));
-        const int lim0 = min(valid0, max(lim_col - t0, 0));
-        const int lim1 = min(valid1, max(lim_col - t0 - 16, 0));
-        if (valid1 == 16 && min_lim - t0 >= 32)
-          tile_core2<false>(S, ka0, ka1, vst0, vst1, vtr, qb, 16, 16, lim0, lim1, q, p.scale_log2);
-        else
-          tile_core2<true>(S, ka0, ka1, vst0, vst1, vtr, qb, valid0, valid1, lim0, lim1, q, p.scale_log2);
+      for (int s = 0; s < NB; ++s) {
+        lds_u8_t* sb = st + s * kPrefixStageBytes;
+        const uint4 (&rs)[2] = ring[h * NB + s];
+        *reinterpret_cast<lds_u32x4_t*>(sb + k_stage(4 * wave + q, n)) =
+            u32x4_t{rs[0].x, rs[0].y, rs[0].z, rs[0].w};
+        *reinterpret_cast<lds_u32x4_t*>(sb + kPrefixKBytes + v_stage(4 * wave + q, n)) =
+            u32x4_t{rs[1].x, rs[1].y, rs[1].z, rs[1].w};
       }
+#pragma unroll
+      for (int s = 0; s < NB; ++s) load(ring[((h + AHEAD) % SETS) * NB + s], NB * (j + AHEAD) + s);
+      __syncthreads();
+
+      int valid[NB], lim[NB];
+      const int t0 = NB * j * 16;
+#pragma unroll
+      for (int s = 0; s < NB; ++s) {
+        const int tb = t0 + 16 * s;
+        valid[s] = max(0, min(16, vis_max - tb));
+        lim[s] = min(valid[s], max(lim_col - tb, 0));
+      }
+      const bool fast = valid[NB - 1] == 16 && min_lim - t0 >= 16 * NB;
+      if (fast)
+        tile_core_nb<false, NB>(S, st, vtr, qb, valid, lim, q, n, p.scale_log2);
+      else
+        tile_core_nb<true, NB>(S, st, vtr, qb, valid, lim, q, n, p.scale_log2);
     }
+  }
   }
 
   // Normalise and write bf16: lane (q, n) holds O[rows 4q+r][dims 16j + n].
