@@ -96,7 +96,7 @@ template <int NT>
 struct MfmaState {
   float m[NT];        // running max of query column n (log2 units), same in all groups
   float l[NT];        // this lane's share of the column sum (tokens 4q..4q+3 of each block)
-  floatx4_t o[NT][8]; // [j]: O[rows 4q+r][dim 8n + j] (tile_core) or [dim 16j + n] (tile_core2)
+  floatx4_t o[NT][8]; // [j]: O[rows 4q+r][dim 8n + j] (tile_core) or [dim 16j + n] (tile_core_nb)
 };
 
 // One 16-token block against NT column tiles that share the K and V
@@ -555,7 +555,7 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
 // its wavefronts share every block: each loads one quarter (four token rows
 // of K and of V, 2 KiB) into a double-buffered LDS stage, and after a
 // barrier every wavefront runs its own tile against the staged blocks, two
-// blocks per barrier through tile_core2.  A block
+// blocks per barrier through tile_core_nb.  A block
 // thus crosses from L2 to the CU once per four tiles, and each wavefront owns
 // whole query rows, so no cross-wavefront merge is needed.  All workgroups of
 // a KV head read the same blocks, so each comes from HBM once and from L2
@@ -774,7 +774,7 @@ __device__ __forceinline__ void group_mfma_body(const PrefixParams& p, int wg_in
 // length), which is the per-column limit the MFMA core already applies.
 // One workgroup owns four tiles (64 rows, wavefront w: tile w) and streams
 // the sequence's blocks once through LDS for all of them, as the
-// shared-prefix pass does, two blocks per barrier through tile_core2; the
+// shared-prefix pass does, two blocks per barrier through tile_core_nb; the
 // stream stops at the workgroup's last visible token.  Each wavefront
 // normalises its rows and writes them as bf16.
 constexpr int kExtendRowsPerWg = 16 * kWaves;
