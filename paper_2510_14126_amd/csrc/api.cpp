@@ -802,7 +802,7 @@ int paged_attn_extend(const pa_kv_pool* pool, const void* q, const int32_t* q_st
   if (max_chunk < 0 || max_chunk > max_context_len)
     return fail(PA_EINVAL, "%s: max_chunk = %d outside [0, max_context_len = %d]", fn, max_chunk,
                 max_context_len);
-  const int64_t groups = ((int64_t)max_chunk * group + 63) / 64;
+  const int64_t groups = ((int64_t)max_chunk * group + pa::kExtendRowsPerWg - 1) / pa::kExtendRowsPerWg;
   if ((int64_t)batch * groups * pool->num_kv_heads > 0x7fffffffLL)
     return fail(PA_EINVAL, "%s: grid too large", fn);
   if (batch == 0 || total_q == 0 || max_chunk == 0) return PA_OK;

@@ -146,6 +146,7 @@ struct ExtendParams {
 };
 hipError_t launch_extend(const ExtendParams& p, int group, hipStream_t stream);
 constexpr int kExtendMaxTokens = 8192;   // context bound of one extend launch
+constexpr int kExtendRowsPerWg = 128;    // query rows (chunk token x head) per extend workgroup
 
 // Append of one token's K and V rows per sequence.
 struct AppendParams {

@@ -257,7 +257,8 @@ static_assert(kExtendStageBlocks % 2 == 0, "blocks go in pairs");
 static_assert(1 <= kExtendLoadAhead && kExtendLoadAhead <= kExtendRingSets, "loads stay in the ring");
 
 // NB 16-token blocks (NB even) staged at st + b * kPrefixStageBytes (K in the
-// k_stage layout, V in the v_stage layout) against one column tile.  The
+// k_stage layout, V in the v_stage layout) against NT column tiles, which
+// share every K and V operand read from LDS.  The
 // QK^T of every block comes first (independent MFMA chains); lane (q, n)
 // then holds the scores of tokens 4r+q of each block for column n, and one
 // online-softmax step covers all NB*16 tokens.  For PV, blocks 2p and 2p+1
@@ -267,79 +268,87 @@ static_assert(1 <= kExtendLoadAhead && kExtendLoadAhead <= kExtendRingSets, "loa
 // per 16 output dims (output column n = dim 16j + n), whose B operand two
 // transposing LDS reads deliver straight from the staged V tiles (vtr is
 // the lane's v_tr offset).  valid[b]: rows of block b that hold tokens of the
-// span (0: an empty block); lim[b]: rows of block b this lane's column may
-// see.  Rows past valid[b] are zeroed in the B operand (their V may be
+// span (0: an empty block); lim[t][b]: rows of block b that column n of
+// tile t may see.  Rows past valid[b] are zeroed in the B operand (their V may be
 // anything, NaN included).
-template <bool TAIL, int NB>
-__device__ __forceinline__ void tile_core_nb(MfmaState<1>& S, const lds_u8_t* st, int vtr,
-                                             const uint4 (&qb)[1][4], const int (&valid)[NB],
-                                             const int (&lim)[NB], int q, int n, float scale_log2) {
+template <bool TAIL, int NB, int NT>
+__device__ __forceinline__ void tile_core_nb(MfmaState<NT>& S, const lds_u8_t* st, int vtr,
+                                             const uint4 (&qb)[NT][4], const int (&valid)[NB],
+                                             const int (&lim)[NT][NB], int q, int n, float scale_log2) {
   static_assert(NB % 2 == 0, "blocks go in pairs through the PV contraction");
   const floatx4_t z = {0.f, 0.f, 0.f, 0.f};
-  // K operands of every block first, then the score MFMAs interleaved over
-  // the blocks so that consecutive MFMAs do not depend on each other.
+  // K operands of every block first (shared by the NT tiles), then the score
+  // MFMAs interleaved over tiles and blocks so that consecutive MFMAs do not
+  // depend on each other.
   u32x4_t ka[NB][4];
 #pragma unroll
   for (int b = 0; b < NB; ++b)
 #pragma unroll
     for (int c = 0; c < 4; ++c)
       ka[b][c] = *reinterpret_cast<const lds_u32x4_t*>(st + b * kPrefixStageBytes + k_stage(k_arow(n), 4 * c + q));
-  floatx4_t a[NB];
+  floatx4_t a[NT][NB];
 #pragma unroll
-  for (int b = 0; b < NB; ++b)
-    a[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[b][0]),
-                                                   __builtin_bit_cast(bf16x8_t, qb[0][0]), z, 0, 0, 0);
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+      a[t][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[b][0]),
+                                                        __builtin_bit_cast(bf16x8_t, qb[t][0]), z, 0, 0, 0);
 #pragma unroll
   for (int c = 1; c < 4; ++c)
 #pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        a[t][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[b][c]),
+                                                          __builtin_bit_cast(bf16x8_t, qb[t][c]), a[t][b], 0, 0, 0);
+
+  // Probabilities of tile t rounded to bf16 (the A operands: element e of
+  // pa[t][p] is the score 8p + e); the column sum uses the same rounded
+  // values, from the packed words by v_dot2 against (1, 1).
+  bf16x8_t pa[NT][NB / 2];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    float sc[4 * NB];
+    bool raise = false;
+#pragma unroll
     for (int b = 0; b < NB; ++b)
-      a[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[b][c]),
-                                                     __builtin_bit_cast(bf16x8_t, qb[0][c]), a[b], 0, 0, 0);
-
-  float sc[4 * NB];
-  bool raise = false;
 #pragma unroll
-  for (int b = 0; b < NB; ++b)
+      for (int r = 0; r < 4; ++r) {
+        float x = a[t][b][r] * scale_log2;
+        if (TAIL && 4 * r + q >= lim[t][b]) x = -__builtin_inff();
+        sc[4 * b + r] = x;
+        raise |= x > S.m[t] + kLazyRescale;
+      }
+    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+      float bmax = sc[0];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      float x = a[b][r] * scale_log2;
-      if (TAIL && 4 * r + q >= lim[b]) x = -__builtin_inff();
-      sc[4 * b + r] = x;
-      raise |= x > S.m[0] + kLazyRescale;
+      for (int e = 1; e < 4 * NB; ++e) bmax = fmaxf(bmax, sc[e]);
+      const float bm = group_max4(bmax);
+      const float mn = bm > S.m[t] + kLazyRescale ? bm : S.m[t];
+      const float alpha = mn == -__builtin_inff() ? 1.f : fast_exp2(S.m[t] - mn);
+      S.l[t] *= alpha;
+      S.m[t] = mn;
+      float ar[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) ar[r] = column_value(alpha, q, r);
+#pragma unroll
+      for (int blk = 0; blk < 8; ++blk)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) S.o[t][blk][r] *= ar[r];
     }
-  if (__builtin_amdgcn_ballot_w64(raise) != 0) {
-    float bmax = sc[0];
-#pragma unroll
-    for (int e = 1; e < 4 * NB; ++e) bmax = fmaxf(bmax, sc[e]);
-    const float bm = group_max4(bmax);
-    const float mn = bm > S.m[0] + kLazyRescale ? bm : S.m[0];
-    const float alpha = mn == -__builtin_inff() ? 1.f : fast_exp2(S.m[0] - mn);
-    S.l[0] *= alpha;
-    S.m[0] = mn;
-    float ar[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) ar[r] = column_value(alpha, q, r);
-#pragma unroll
-    for (int blk = 0; blk < 8; ++blk)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) S.o[0][blk][r] *= ar[r];
-  }
 
-  const float mref = S.m[0] == -__builtin_inff() ? 0.f : S.m[0];
-  // Probabilities rounded to bf16 (the A operands: element e of pa[p] is
-  // sc[8p + e]); the column sum uses the same rounded values, from the
-  // packed words by v_dot2 against (1, 1).
-  bf16x8_t pa[NB / 2];
-  float lsum = 0.f;
+    const float mref = S.m[t] == -__builtin_inff() ? 0.f : S.m[t];
+    float lsum = 0.f;
 #pragma unroll
-  for (int pp = 0; pp < NB / 2; ++pp) {
+    for (int pp = 0; pp < NB / 2; ++pp) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) pa[pp][e] = (__bf16)fast_exp2(sc[8 * pp + e] - mref);
-    const u32x4_t pw = __builtin_bit_cast(u32x4_t, pa[pp]);
+      for (int e = 0; e < 8; ++e) pa[t][pp][e] = (__bf16)fast_exp2(sc[8 * pp + e] - mref);
+      const u32x4_t pw = __builtin_bit_cast(u32x4_t, pa[t][pp]);
 #pragma unroll
-    for (int w = 0; w < 4; ++w) lsum = dot2_bf16(pw[w], 0x3F803F80u, lsum);
+      for (int w = 0; w < 4; ++w) lsum = dot2_bf16(pw[w], 0x3F803F80u, lsum);
+    }
+    S.l[t] += lsum;
   }
-  S.l[0] += lsum;
 
   // Element e of a block's B words is its token 4e + q.
   uint32_t mlo[NB], mhi[NB];
@@ -352,6 +361,7 @@ __device__ __forceinline__ void tile_core_nb(MfmaState<1>& S, const lds_u8_t* st
       mhi[b] = (q + 8 < valid[b] ? 0xffffu : 0u) | (q + 12 < valid[b] ? 0xffff0000u : 0u);
     }
   }
+  // Each B operand (two transposing reads) serves the NT tiles.
 #pragma unroll
   for (int pp = 0; pp < NB / 2; ++pp) {
     const lds_u8_t* v0 = st + (2 * pp) * kPrefixStageBytes + kPrefixKBytes;
@@ -365,8 +375,10 @@ __device__ __forceinline__ void tile_core_nb(MfmaState<1>& S, const lds_u8_t* st
           uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(v1 + off)));
       const u32x4_t vb = {b0.x & mlo[2 * pp], b0.y & mhi[2 * pp], b1.x & mlo[2 * pp + 1],
                           b1.y & mhi[2 * pp + 1]};
-      S.o[0][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[pp], __builtin_bit_cast(bf16x8_t, vb),
-                                                          S.o[0][j], 0, 0, 0);
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        S.o[t][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[t][pp], __builtin_bit_cast(bf16x8_t, vb),
+                                                            S.o[t][j], 0, 0, 0);
     }
   }
 }
@@ -672,7 +684,7 @@ __device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, c
         load(ring[(2 * h + kRing - 2) % kRing], 2 * j + kRing - 2);
         load(ring[(2 * h + kRing - 1) % kRing], 2 * j + kRing - 1);
         __syncthreads();
-        int valid[NB], lim[NB];
+        int valid[NB], lim[1][NB];
         bool fast = true;
 #pragma unroll
         for (int s = 0; s < NB; ++s) {
@@ -680,7 +692,7 @@ __device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, c
           const bool has = i < nblk;
           const int tb = has ? start + block_of(i) * 16 : end;
           valid[s] = has ? min(16, end - tb) : 0;
-          lim[s] = min(valid[s], max(ctx - tb, 0));
+          lim[0][s] = min(valid[s], max(ctx - tb, 0));
           fast = fast && valid[s] == 16 && min_ctx - tb >= 16;
         }
         if (fast)
@@ -772,12 +784,14 @@ __device__ __forceinline__ void group_mfma_body(const PrefixParams& p, int wg_in
 // head j) pairs of sequence b form rows R = i*G + j of dense 16-row tiles;
 // row R sees the tokens 0 .. n - L + i (n: context with the chunk, L: chunk
 // length), which is the per-column limit the MFMA core already applies.
-// One workgroup owns four tiles (64 rows, wavefront w: tile w) and streams
-// the sequence's blocks once through LDS for all of them, as the
-// shared-prefix pass does, two blocks per barrier through tile_core_nb; the
-// stream stops at the workgroup's last visible token.  Each wavefront
-// normalises its rows and writes them as bf16.
-constexpr int kExtendRowsPerWg = 16 * kWaves;
+// One workgroup owns kExtendRowsPerWg rows, kExtendTilesPerWave adjacent
+// tiles per wavefront, and streams the sequence's blocks once through LDS
+// for all of them, as the shared-prefix pass does, two blocks per barrier
+// through tile_core_nb, whose K and V operand reads serve all of a
+// wavefront's tiles; the stream stops at the workgroup's last visible token.
+// Each wavefront normalises its rows and writes them as bf16.
+constexpr int kExtendTilesPerWave = kExtendRowsPerWg / (16 * kWaves);
+static_assert(kExtendTilesPerWave * 16 * kWaves == kExtendRowsPerWg, "whole tiles per wavefront");
 constexpr int kExtendIdOffset = 2 * kExtendStageBlocks * kPrefixStageBytes;   // after two stages
 constexpr int kExtendLdsBytes = kExtendIdOffset + kExtendMaxTokens / 16 * 4;   // + the block ids
 
@@ -803,7 +817,8 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
   L = qs + L > p.total_q ? (p.total_q > qs ? p.total_q - qs : 0) : L;
   const int rows = L * G;
   if (grp * kExtendRowsPerWg >= rows) return;          // whole workgroup: no rows here
-  const int row0 = grp * kExtendRowsPerWg + 16 * wave; // this wavefront's tile
+  constexpr int NT = kExtendTilesPerWave;
+  const int row0 = grp * kExtendRowsPerWg + 16 * NT * wave;   // this wavefront's first tile
   const int first = ctx - L;                           // position of chunk token 0
 
   // Tokens the workgroup needs: up to its last row's position.
@@ -823,28 +838,36 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
   }
   auto block_id = [&](int i) { return __builtin_amdgcn_readfirstlane(ids[i]); };
 
-  // Column n is row R = row0 + n: chunk token R / G, query head g*G + R % G.
-  uint4 qb[1][4];
-  int lim_col;       // tokens this column sees
-  int min_lim;       // fewest tokens any live column of the tile sees
+  // Column n of tile t is row R = row0 + 16t + n: chunk token R / G, query
+  // head g*G + R % G.
+  uint4 qb[NT][4];
+  int lim_col[NT];   // tokens column n of tile t sees
+  int min_lim;       // fewest tokens any live column of the wavefront's tiles sees
   {
-    const int R = row0 + n;
-    const bool ok = R < rows;
-    const int i = ok ? R / G : 0;
-    const uint16_t* qrow = p.q + ((size_t)(qs + i) * p.num_q_heads + g * G + R % G) * kD;
+    int for_min = 0x3fffffff;
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
-      qb[0][s] = ok ? *reinterpret_cast<const uint4*>(qrow + (4 * s + q) * 8) : make_uint4(0, 0, 0, 0);
-    lim_col = ok ? first + i + 1 : 0;
-    const int for_min = ok ? lim_col : 0x3fffffff;
+    for (int t = 0; t < NT; ++t) {
+      const int R = row0 + 16 * t + n;
+      const bool ok = R < rows;
+      const int i = ok ? R / G : 0;
+      const uint16_t* qrow = p.q + ((size_t)(qs + i) * p.num_q_heads + g * G + R % G) * kD;
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        qb[t][s] = ok ? *reinterpret_cast<const uint4*>(qrow + (4 * s + q) * 8) : make_uint4(0, 0, 0, 0);
+      lim_col[t] = ok ? first + i + 1 : 0;
+      for_min = ok ? min(for_min, lim_col[t]) : for_min;
+    }
     min_lim = __builtin_amdgcn_readfirstlane(-(int)group_max4(row_max16(-(float)for_min)));
   }
 
-  MfmaState<1> S;
-  S.m[0] = -__builtin_inff();
-  S.l[0] = 0.f;
+  MfmaState<NT> S;
 #pragma unroll
-  for (int blk = 0; blk < 8; ++blk) S.o[0][blk] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < NT; ++t) {
+    S.m[t] = -__builtin_inff();
+    S.l[t] = 0.f;
+#pragma unroll
+    for (int blk = 0; blk < 8; ++blk) S.o[t][blk] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+  }
 
   constexpr size_t kTileElems = 16 * kD;
   const size_t blk_stride = (size_t)p.num_kv_heads * kTileElems;
@@ -896,13 +919,14 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
       for (int s = 0; s < NB; ++s) load(ring[((h + AHEAD) % SETS) * NB + s], NB * (j + AHEAD) + s);
       __syncthreads();
 
-      int valid[NB], lim[NB];
+      int valid[NB], lim[NT][NB];
       const int t0 = NB * j * 16;
 #pragma unroll
       for (int s = 0; s < NB; ++s) {
         const int tb = t0 + 16 * s;
         valid[s] = max(0, min(16, vis_max - tb));
-        lim[s] = min(valid[s], max(lim_col - tb, 0));
+#pragma unroll
+        for (int t = 0; t < NT; ++t) lim[t][s] = min(valid[s], max(lim_col[t] - tb, 0));
       }
       const bool fast = valid[NB - 1] == 16 && min_lim - t0 >= 16 * NB;
       if (fast)
@@ -913,17 +937,20 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
   }
   }
 
-  // Normalise and write bf16: lane (q, n) holds O[rows 4q+r][dims 16j + n].
-  const float lcol = group_sum4(S.l[0]);
-  const float inv = lcol > 0.f ? 1.0f / lcol : 0.f;
+  // Normalise and write bf16: lane (q, n) holds O[rows 4q+r of tile t][dims 16j + n].
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int R = row0 + 4 * q + r;
-    const float f = column_value(inv, q, r);
-    if (R < rows) {
-      uint16_t* orow = p.out + ((size_t)(qs + R / G) * p.num_q_heads + g * G + R % G) * kD + n;
+  for (int t = 0; t < NT; ++t) {
+    const float lcol = group_sum4(S.l[t]);
+    const float inv = lcol > 0.f ? 1.0f / lcol : 0.f;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) orow[16 * j] = (uint16_t)bf16_rne(S.o[0][j][r] * f);
+    for (int r = 0; r < 4; ++r) {
+      const int R = row0 + 16 * t + 4 * q + r;
+      const float f = column_value(inv, q, r);
+      if (R < rows) {
+        uint16_t* orow = p.out + ((size_t)(qs + R / G) * p.num_q_heads + g * G + R % G) * kD + n;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) orow[16 * j] = (uint16_t)bf16_rne(S.o[t][j][r] * f);
+      }
     }
   }
 }
