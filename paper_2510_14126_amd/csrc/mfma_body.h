@@ -791,6 +791,7 @@ __device__ __forceinline__ void group_mfma_body(const PrefixParams& p, int wg_in
 // wavefront's tiles; the stream stops at the workgroup's last visible token.
 // Each wavefront normalises its rows and writes them as bf16.
 constexpr int kExtendTilesPerWave = kExtendRowsPerWg / (16 * kWaves);
+template <bool B> struct BoolTag { static constexpr bool value = B; };
 static_assert(kExtendTilesPerWave * 16 * kWaves == kExtendRowsPerWg, "whole tiles per wavefront");
 constexpr int kExtendIdOffset = 2 * kExtendStageBlocks * kPrefixStageBytes;   // after two stages
 constexpr int kExtendLdsBytes = kExtendIdOffset + kExtendMaxTokens / 16 * 4;   // + the block ids
@@ -842,9 +843,7 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
   // head g*G + R % G.
   uint4 qb[NT][4];
   int lim_col[NT];   // tokens column n of tile t sees
-  int min_lim;       // fewest tokens any live column of the wavefront's tiles sees
   {
-    int for_min = 0x3fffffff;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       const int R = row0 + 16 * t + n;
@@ -855,9 +854,7 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
       for (int s = 0; s < 4; ++s)
         qb[t][s] = ok ? *reinterpret_cast<const uint4*>(qrow + (4 * s + q) * 8) : make_uint4(0, 0, 0, 0);
       lim_col[t] = ok ? first + i + 1 : 0;
-      for_min = ok ? min(for_min, lim_col[t]) : for_min;
     }
-    min_lim = __builtin_amdgcn_readfirstlane(-(int)group_max4(row_max16(-(float)for_min)));
   }
 
   MfmaState<NT> S;
@@ -900,11 +897,23 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
 #pragma unroll
   for (int s = 0; s < AHEAD * NB; ++s) load(ring[s], s);
   const int nit = (nblk + NB - 1) / NB;
-  for (int j0 = 0; j0 < nit; j0 += SETS) {
+  // Stages 0 .. nfast-1 are wholly visible to every row of the workgroup
+  // (its first row sees the fewest tokens) and run unmasked in a loop of
+  // their own; the rest, up to the causal diagonal, run masked in a second
+  // loop.  One core per loop keeps the compiler from copying the output
+  // accumulators where the two cores' paths would otherwise merge.  nfast
+  // is a multiple of SETS so that both loops find stage j in slot set
+  // j % SETS.
+  const int wg_min_lim = first + grp * kExtendRowsPerWg / G + 1;
+  int nfast = min(wg_min_lim, vis_max) / (16 * NB);
+  nfast = min(nfast - nfast % SETS, nit);
+  auto stream = [&](auto tail, int jb, int je) {
+  constexpr bool TAIL = decltype(tail)::value;
+  for (int j0 = jb; j0 < je; j0 += SETS) {
 #pragma unroll
   for (int h = 0; h < SETS; ++h) {
     const int j = j0 + h;
-    if (j < nit) {                              // uniform over the workgroup
+    if (j < je) {                               // uniform over the workgroup
       lds_u8_t* st = smem + (j & 1) * NB * kPrefixStageBytes;
 #pragma unroll
       for (int s = 0; s < NB; ++s) {
@@ -928,14 +937,13 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
 #pragma unroll
         for (int t = 0; t < NT; ++t) lim[t][s] = min(valid[s], max(lim_col[t] - tb, 0));
       }
-      const bool fast = valid[NB - 1] == 16 && min_lim - t0 >= 16 * NB;
-      if (fast)
-        tile_core_nb<false, NB>(S, st, vtr, qb, valid, lim, q, n, p.scale_log2);
-      else
-        tile_core_nb<true, NB>(S, st, vtr, qb, valid, lim, q, n, p.scale_log2);
+      tile_core_nb<TAIL, NB>(S, st, vtr, qb, valid, lim, q, n, p.scale_log2);
     }
   }
   }
+  };
+  stream(BoolTag<false>{}, 0, nfast);
+  stream(BoolTag<true>{}, nfast, nit);
 
   // Normalise and write bf16: lane (q, n) holds O[rows 4q+r of tile t][dims 16j + n].
 #pragma unroll
