@@ -86,6 +86,10 @@ CASES = [
     ("one-token chunks", [5, 300, 1000], [1, 1, 1]),
     ("ragged with an empty chunk", [40, 10, 21, 77], [3, 0, 21, 64]),
     ("chunk across many tiles", [700], [300]),
+    # unmasked-stage count even, odd (rounded down to the ring's two slot
+    # sets) and equal to the whole stream, and long chunks whose workgroups
+    # cross the causal diagonal at different stages
+    ("diagonal and ring parity", [64, 96, 1024, 1056, 333], [1, 1, 200, 37, 129]),
 ]
 
 
