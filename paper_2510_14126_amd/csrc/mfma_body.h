@@ -245,8 +245,10 @@ constexpr int kPrefixStageBytes = kPrefixKBytes + 16 * kD * 2;
 // kExtendRingSets sets of slots, each stage loaded kExtendLoadAhead stages
 // before it is published (1 <= AHEAD <= SETS; stage j in set j % SETS).
 // Measured fastest: the prefix pass as described (the generic loop at the
-// same depth was 4% slower on the generator batch), extend at (2, 2, 2),
-// where it needs 162 VGPRs and runs three wavefronts per SIMD.
+// same depth was 4% slower on the generator batch), extend at (2, 2, 2)
+// (with one tile per wavefront that form needed 162 VGPRs and ran three
+// wavefronts per SIMD; two tiles per wavefront need 218 and run two, and
+// are faster).
 constexpr int kPrefixStageBlocks = 2;
 constexpr int kPrefixRing = 4;
 constexpr int kExtendStageBlocks = 2;
