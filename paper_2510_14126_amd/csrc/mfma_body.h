@@ -272,8 +272,12 @@ static_assert(1 <= kExtendLoadAhead && kExtendLoadAhead <= kExtendRingSets, "loa
 // the lane's v_tr offset).  valid[b]: rows of block b that hold tokens of the
 // span (0: an empty block); lim[t][b]: rows of block b that column n of
 // tile t may see.  Rows past valid[b] are zeroed in the B operand (their V may be
-// anything, NaN included).
-template <bool TAIL, int NB, int NT>
+// anything, NaN included).  With FOLD (scale_log2 >= 0 required) the scale
+// is applied inside the exponent's FMA, and the running-max test uses the
+// lane's largest unmasked raw score times the scale (the same value as the
+// largest scaled score, since multiplying by a non-negative number keeps
+// the order).
+template <bool TAIL, int NB, int NT, bool FOLD = false>
 __device__ __forceinline__ void tile_core_nb(MfmaState<NT>& S, const lds_u8_t* st, int vtr,
                                              const uint4 (&qb)[NT][4], const int (&valid)[NB],
                                              const int (&lim)[NT][NB], int q, int n, float scale_log2) {
@@ -310,21 +314,34 @@ __device__ __forceinline__ void tile_core_nb(MfmaState<NT>& S, const lds_u8_t* s
   bf16x8_t pa[NT][NB / 2];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    float sc[4 * NB];
+    float sc[4 * NB];   // scaled scores, or raw ones with FOLD
     bool raise = false;
+    float mx = -__builtin_inff();   // FOLD: the lane's largest unmasked raw score
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        float x = a[t][b][r] * scale_log2;
-        if (TAIL && 4 * r + q >= lim[t][b]) x = -__builtin_inff();
-        sc[4 * b + r] = x;
-        raise |= x > S.m[t] + kLazyRescale;
+        if constexpr (FOLD) {
+          const float raw = a[t][b][r];
+          sc[4 * b + r] = raw;
+          if (!TAIL || 4 * r + q < lim[t][b]) mx = fmaxf(mx, raw);
+        } else {
+          float x = a[t][b][r] * scale_log2;
+          if (TAIL && 4 * r + q >= lim[t][b]) x = -__builtin_inff();
+          sc[4 * b + r] = x;
+          raise |= x > S.m[t] + kLazyRescale;
+        }
       }
+    const float xmax = mx * scale_log2;   // FOLD only (NaN when all are masked and the scale is 0)
+    if constexpr (FOLD) raise = xmax > S.m[t] + kLazyRescale;
     if (__builtin_amdgcn_ballot_w64(raise) != 0) {
       float bmax = sc[0];
+      if constexpr (FOLD) {
+        bmax = xmax;
+      } else {
 #pragma unroll
-      for (int e = 1; e < 4 * NB; ++e) bmax = fmaxf(bmax, sc[e]);
+        for (int e = 1; e < 4 * NB; ++e) bmax = fmaxf(bmax, sc[e]);
+      }
       const float bm = group_max4(bmax);
       const float mn = bm > S.m[t] + kLazyRescale ? bm : S.m[t];
       const float alpha = mn == -__builtin_inff() ? 1.f : fast_exp2(S.m[t] - mn);
@@ -344,7 +361,17 @@ __device__ __forceinline__ void tile_core_nb(MfmaState<NT>& S, const lds_u8_t* s
 #pragma unroll
     for (int pp = 0; pp < NB / 2; ++pp) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pa[t][pp][e] = (__bf16)fast_exp2(sc[8 * pp + e] - mref);
+      for (int e = 0; e < 8; ++e) {
+        float ex;
+        if constexpr (FOLD) {
+          ex = fmaf(sc[8 * pp + e], scale_log2, -mref);
+          // element e is token 4(e % 4) + q of block 2pp + e / 4
+          if (TAIL && 4 * (e & 3) + q >= lim[t][2 * pp + (e >> 2)]) ex = -__builtin_inff();
+        } else {
+          ex = sc[8 * pp + e] - mref;
+        }
+        pa[t][pp][e] = (__bf16)fast_exp2(ex);
+      }
       const u32x4_t pw = __builtin_bit_cast(u32x4_t, pa[t][pp]);
 #pragma unroll
       for (int w = 0; w < 4; ++w) lsum = dot2_bf16(pw[w], 0x3F803F80u, lsum);
@@ -842,7 +869,11 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
   auto block_id = [&](int i) { return __builtin_amdgcn_readfirstlane(ids[i]); };
 
   // Column n of tile t is row R = row0 + 16t + n: chunk token R / G, query
-  // head g*G + R % G.
+  // head g*G + R % G.  A negative scale goes into the sign of Q (bf16
+  // negation is exact, and so is the negation of every score), so the core
+  // folds a non-negative scale into its exponent.
+  const uint32_t qflip = p.scale_log2 < 0.f ? 0x80008000u : 0u;
+  const float scale_abs = fabsf(p.scale_log2);
   uint4 qb[NT][4];
   int lim_col[NT];   // tokens column n of tile t sees
   {
@@ -853,8 +884,11 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
       const int i = ok ? R / G : 0;
       const uint16_t* qrow = p.q + ((size_t)(qs + i) * p.num_q_heads + g * G + R % G) * kD;
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
-        qb[t][s] = ok ? *reinterpret_cast<const uint4*>(qrow + (4 * s + q) * 8) : make_uint4(0, 0, 0, 0);
+      for (int s = 0; s < 4; ++s) {
+        uint4 w = ok ? *reinterpret_cast<const uint4*>(qrow + (4 * s + q) * 8) : make_uint4(0, 0, 0, 0);
+        w.x ^= qflip; w.y ^= qflip; w.z ^= qflip; w.w ^= qflip;
+        qb[t][s] = w;
+      }
       lim_col[t] = ok ? first + i + 1 : 0;
     }
   }
@@ -939,7 +973,7 @@ __device__ __forceinline__ void extend_mfma_body(const ExtendParams& p, int wg_i
 #pragma unroll
         for (int t = 0; t < NT; ++t) lim[t][s] = min(valid[s], max(lim_col[t] - tb, 0));
       }
-      tile_core_nb<TAIL, NB>(S, st, vtr, qb, valid, lim, q, n, p.scale_log2);
+      tile_core_nb<TAIL, NB, NT, true>(S, st, vtr, qb, valid, lim, q, n, scale_abs);
     }
   }
   }

@@ -122,3 +122,14 @@ def test_one_token_extend_matches_gpu_decode():
     assert compare(ext, ref).passed and compare(dec, ref).passed
     diff = np.abs(ext.astype(np.int32) - dec.astype(np.int32))
     say(f"extend vs decode: max bf16 ulp difference {int(diff.max())}")
+
+
+@pytest.mark.parametrize("factor", [-1.0, 0.0], ids=["negative", "zero"])
+def test_extend_scale_sign(factor):
+    """A negative scale (carried by the sign of Q inside the kernel) and a zero
+    scale (uniform weights over the visible tokens), with masked tails."""
+    ctx, chunk = [333, 64, 1056], [129, 1, 37]
+    say(f"extend scale x{factor}: ctx={ctx} chunk={chunk}")
+    w, q, q_start = make_extend(71, ctx, chunk, poison=True)
+    w.scale = float(w.scale) * factor
+    check(w, q, q_start, f"scale x{factor}")
