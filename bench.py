@@ -4,10 +4,16 @@ A step is one pass of the whole hot path over one batch: the split-KV decode
 (for batches that share a schema prefix, the one-launch cascade: a
 matrix-core pass over the shared prefix for all query rows plus the
 per-sequence decode of the tokens after it) followed by the cross-split
-reduce, for every sequence and head of the batch.  The default workload is
-the SQL-generator stage (batch 64, 32 query / 8 KV heads, head_dim 128, a
-2048-token schema prefix shared by every sequence plus a unique 64..512-token
-suffix, 16-token blocks), with seeded synthetic bf16 N(0,1) inputs.
+reduce, for every sequence and head of the batch.
+
+Workloads (seeded synthetic bf16 N(0,1) inputs, 16-token blocks, one layer):
+the headline line is the long-context stage pool (batch 128, 64 query / 8 KV
+heads, head_dim 128, contexts 8192..32768 tokens with a shared 4096-token
+prefix, 512-token split-KV partitions), the largest of the five stage-shaped
+batches; the same line carries a ``per_config`` entry for each of the other
+four (tiny, SQL generator, SQL error fixer, shared pool), each with its own
+step time, roofline fraction, parity spot check and CPU-oracle baseline.
+``--config k`` measures batch k alone.
 
 Timing: the pools and queries are replicated R times in HBM (R copies of the
 same data at different addresses, like R layers of a model) and consecutive
@@ -46,7 +52,15 @@ KERNEL_SOURCES = {
     "decode_mfma": [_CSRC + f for f in ("decode_mfma.hip", "mfma_body.h", "pa_device.h", "kernels.h")],
     "cascade": [_CSRC + f for f in ("cascade.hip", "valu_body.h", "mfma_body.h", "pa_device.h",
                                     "kernels.h")],
+    "reduce": [_CSRC + f for f in ("reduce.hip", "pa_device.h", "kernels.h")],
+    "append": [_CSRC + f for f in ("append.hip", "pa_device.h", "kernels.h")],
+    "extend": [_CSRC + f for f in ("extend.hip", "mfma_body.h", "pa_device.h", "kernels.h")],
+    "gather_tiles": [_CSRC + f for f in ("gather_tiles.hip", "pa_device.h", "kernels.h")],
+    "stream_copy": [_CSRC + f for f in ("stream_copy.hip", "kernels.h")],
 }
+LIBRARY_PATH = os.path.join(ROOT, "paper_2510_14126_amd", "libpaged_attn.so")
+HEADLINE_CONFIG = 5            # the largest single-GPU stage batch (long-context pool)
+PER_CONFIG = (1, 2, 3, 4)      # the other stage batches, reported in the same line
 # Split-KV partition sizes used when --partition-size is not given.  The
 # long-context pool states 512-token partitions; the other workloads state
 # none and use the size that measured fastest on them with the host-built
@@ -62,6 +76,28 @@ DEFAULT_PREFIX_PARTITION = {2: 512, 3: 1024, 5: 512}
 def default_prefix_partition(config: int, prefix_len: int) -> int:
     size = DEFAULT_PREFIX_PARTITION.get(config, 1024)
     return max(16, min(size, -(-prefix_len // 16) * 16))
+
+
+def launch_configuration(k, w, partition_size=None, prefix_partition_size=None, cascade="auto",
+                         groups="auto"):
+    """Partition size and PagedBatch keywords of the launch this benchmark
+    times on workload k: the stated or measured-fastest partition size; the
+    shared-prefix cascade when the batch shares a prefix; request groups when
+    its sequences also share tokens per group after the prefix."""
+    from workloads import group_starts
+    S = partition_size or DEFAULT_PARTITION.get(k, w.partition_size)
+    L = 16 * int(w.meta.get("prefix_blocks", 0))
+    if cascade == "off" or (cascade == "auto" and L == 0):
+        L = 0
+    M = 16 * int(w.meta.get("mid_blocks", 0)) if "groups" in w.meta else 0
+    if groups == "on" and (M == 0 or L == 0):
+        raise SystemExit("--groups on: this workload has no groups sharing tokens after the prefix")
+    kw = {}
+    if L:
+        kw = dict(prefix_len=L, prefix_partition_size=prefix_partition_size or default_prefix_partition(k, L))
+        if M and groups != "off":
+            kw.update(group_start=group_starts(w), group_len=M)
+    return S, kw
 
 
 def decode_kernel_of(w, prefix_len: int = 0) -> str:
@@ -86,6 +122,43 @@ def kernel_source_hash(kernel: str = "decode_valu") -> str:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
+
+
+def library_source_hash() -> str:
+    """Hash of every source of the library (kernels, C ABI, header)."""
+    csrc = os.path.join(ROOT, _CSRC)
+    files = sorted(os.path.join(csrc, f) for f in os.listdir(csrc))
+    files.append(os.path.join(ROOT, "include", "paged_attn.h"))
+    h = hashlib.sha256()
+    for p in files:
+        with open(p, "rb") as f:
+            h.update(os.path.basename(p).encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def source_stamp() -> dict:
+    """What a profiled run was built from: written by the run itself
+    (--profile-loop --stamp) and checked when its results are ingested."""
+    lib = None
+    if os.path.exists(LIBRARY_PATH):
+        with open(LIBRARY_PATH, "rb") as f:
+            lib = hashlib.sha256(f.read()).hexdigest()[:16]
+    return {"library_source_sha256_16": library_source_hash(),
+            "kernel_source_sha256_16": {k: kernel_source_hash(k) for k in KERNEL_SOURCES},
+            "library_sha256_16": lib}
+
+
+def checked_stamp(path) -> dict:
+    """The stamp of a profiled run; refuses one taken on other sources."""
+    if not path:
+        raise SystemExit("ingest needs --stamp: the source stamp the profiled run wrote")
+    with open(path) as f:
+        st = json.load(f)
+    cur = library_source_hash()
+    if st.get("library_source_sha256_16") != cur:
+        raise SystemExit(f"profile stamp {st.get('library_source_sha256_16')} does not match the "
+                         f"current library sources {cur}: profile again")
+    return st
 
 
 def byte_accounting(w):
@@ -128,16 +201,20 @@ def cpu_baseline(w, alg_bytes, min_seconds=10.0, logical_bytes=None):
 
     The oracle runs over the batch's sequences in a process pool (one BLAS
     thread per worker) and the step is repeated until min_seconds pass.
+    Called before the process touches the GPU: the pool is forked.  Workers:
+    the CPUs this process may use, at most 16, the host share of one GPU.
     """
     import multiprocessing as mp
     global _W
     _W = w
-    cores = max(1, min(16, len(os.sched_getaffinity(0))))
+    affinity = len(os.sched_getaffinity(0))
+    cores = max(1, min(16, affinity))
     chunks = [list(range(i, w.batch, cores)) for i in range(cores)]
     chunks = [c for c in chunks if c]
     ctx = mp.get_context("fork")
     steps = 0
-    with ctx.Pool(len(chunks)) as pool:
+    pool = ctx.Pool(len(chunks))
+    try:
         pool.map(_oracle_chunk, [chunks[0][:1]])                   # workers up
         t0 = time.perf_counter()
         while True:
@@ -146,6 +223,10 @@ def cpu_baseline(w, alg_bytes, min_seconds=10.0, logical_bytes=None):
             el = time.perf_counter() - t0
             if el >= min_seconds:
                 break
+    finally:
+        pool.close()
+        pool.join()
+    _W = None
     sec_per_step = el / steps
     return {"value": round(alg_bytes / sec_per_step / 1e9, 4), "unit": "GB/s", "cores": len(chunks),
             "kind": "oracle", "sample": f"{steps} full decode steps of the same batch "
@@ -154,7 +235,7 @@ def cpu_baseline(w, alg_bytes, min_seconds=10.0, logical_bytes=None):
             "decode_steps_per_s": round(1.0 / sec_per_step, 3),
             "logical_kv_gbps": (round(logical_bytes / sec_per_step / 1e9, 4)
                                 if logical_bytes else None),
-            "cpu_model": _cpu_model(), "numpy": np.__version__}
+            "affinity_cpus": affinity, "cpu_model": _cpu_model(), "numpy": np.__version__}
 
 
 # ------------------------------------------------------------------ traffic
@@ -173,7 +254,7 @@ def traffic_from_profiles(workload_name, kernel="decode_valu"):
     return float(m_tr.group(1))
 
 
-def ingest_counters(fetch_csv, write_csv, workload_name, kernel_prefix, command_note):
+def ingest_counters(fetch_csv, write_csv, workload_name, kernel_prefix, command_note, stamp):
     """Write the traffic summary from two rocprofv3 --pmc CSVs (FETCH_SIZE, WRITE_SIZE).
 
     Each counter is scaled by what it reads for the calibration copy of
@@ -216,11 +297,12 @@ def ingest_counters(fetch_csv, write_csv, workload_name, kernel_prefix, command_
                  f"algorithmic_bytes_per_launch: {alg}\n"
                  f"traffic_bytes_per_launch: {fetched + written:.6e}\n"
                  f"traffic_over_algorithmic: {(fetched + written) / alg:.4f}\n"
-                 f"kernel_source_sha256_16: {kernel_source_hash(kernel_prefix)}\n")
+                 f"kernel_source_sha256_16: {stamp['kernel_source_sha256_16'][kernel_prefix]}\n"
+                 f"library_source_sha256_16: {stamp['library_source_sha256_16']}\n")
     print(out)
 
 
-def ingest_sq(csv_paths, workload_name, kernel_substr, command_note, stem):
+def ingest_sq(csv_paths, workload_name, kernel_substr, command_note, stem, stamp):
     """Write a per-dispatch summary of SQ (shader sequencer) counters for one kernel."""
     import csv
     import collections
@@ -265,10 +347,11 @@ def ingest_sq(csv_paths, workload_name, kernel_substr, command_note, stem):
         for c in sorted(m):
             fh.write(f"| {c} | {m[c]:,.0f} |\n")
         fh.write("\n| derived | value |\n|---|---|\n" + "\n".join(lines) + "\n")
+        fh.write(f"\nlibrary_source_sha256_16: {stamp['library_source_sha256_16']}\n")
     print(out)
 
 
-def ingest_stats(stats_csv, workload_name, command_note, stem=None):
+def ingest_stats(stats_csv, workload_name, command_note, stamp, stem=None):
     """Write the kernel-duration summary from a rocprofv3 --stats kernel_stats.csv."""
     import csv
     rows = list(csv.DictReader(open(stats_csv)))
@@ -280,8 +363,9 @@ def ingest_stats(stats_csv, workload_name, command_note, stem=None):
         for r in rows:
             fh.write(f"| `{r['Name'][:90]}` | {r['Calls']} | {float(r['AverageNs'])/1e3:.2f} | "
                      f"{float(r['MinNs'])/1e3:.2f} | {float(r['MaxNs'])/1e3:.2f} | {float(r['Percentage']):.1f}% |\n")
-        fh.write("".join(f"\nkernel_source_sha256_16 ({k}): {kernel_source_hash(k)}"
-                         for k in KERNEL_SOURCES) + "\n")
+        fh.write("".join(f"\nkernel_source_sha256_16 ({k}): {h}"
+                         for k, h in stamp["kernel_source_sha256_16"].items()) +
+                 f"\nlibrary_source_sha256_16: {stamp['library_source_sha256_16']}\n")
     print(out)
 
 
@@ -297,17 +381,34 @@ def extend_chunks(w) -> np.ndarray:
     return np.maximum(w.context_lens.astype(np.int64) - shared, 1).astype(np.int32)
 
 
+def extend_inputs(w):
+    """(chunk lengths, q_start, bf16 query rows) of the extend batch timed here:
+    each sequence's chunk as ``extend_chunks``, queries N(0,1) from seed 4242."""
+    from workloads import f32_to_bf16_bits
+    chunk = extend_chunks(w)
+    q_start = np.concatenate([[0], np.cumsum(chunk)]).astype(np.int32)
+    rng = np.random.default_rng(4242)
+    q = f32_to_bf16_bits(rng.standard_normal((int(q_start[-1]), w.num_q_heads, w.head_dim),
+                                             dtype=np.float32))
+    return chunk, q_start, q
+
+
+def extend_flops(w, chunk) -> int:
+    """Causal flops of one extend call: 4 Hq D per (row, visible token)."""
+    ctx = w.context_lens.astype(np.int64)
+    L = chunk.astype(np.int64)
+    # row i of sequence b sees n - L + i + 1 tokens: the sum over i of a chunk
+    vis = L * (ctx - L) + L * (L + 1) // 2
+    return int(4 * w.num_q_heads * w.head_dim * int(vis.sum()))
+
+
 def run_extend(w, base, reps, R, K, stream, sh, binding):
     """Time paged_attn_extend on the workload's batch and spot-check two sequences."""
     import torch
-    from workloads import f32_to_bf16_bits
     if w.head_dim != 128 or w.max_context_len > 8192:
         return {"skipped": "extend needs head_dim 128 and contexts up to 8192 tokens"}
-    chunk = extend_chunks(w)
-    q_start = np.concatenate([[0], np.cumsum(chunk)]).astype(np.int32)
+    chunk, q_start, q = extend_inputs(w)
     total = int(q_start[-1])
-    rng = np.random.default_rng(4242)
-    q = f32_to_bf16_bits(rng.standard_normal((total, w.num_q_heads, w.head_dim), dtype=np.float32))
     dev = base.q.device
     q_dev = torch.from_numpy(q.view(np.int16)).to(dev)
     qs_dev = torch.from_numpy(q_start).to(dev)
@@ -328,12 +429,7 @@ def run_extend(w, base, reps, R, K, stream, sh, binding):
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / n_calls
-    ctx = w.context_lens.astype(np.int64)
-    flops = 0
-    for b in range(w.batch):
-        L, n = int(chunk[b]), int(ctx[b])
-        vis = np.arange(n - L + 1, n + 1, dtype=np.int64)        # tokens each chunk row sees
-        flops += 4 * w.num_q_heads * w.head_dim * int(vis.sum())
+    flops = extend_flops(w, chunk)
     from workloads import touched_slots
     alg_bytes = touched_slots(w) * w.bytes_per_token + 2 * total * w.num_q_heads * w.head_dim * 2
     # parity spot check on the first and the longest-chunk sequence
@@ -347,6 +443,7 @@ def run_extend(w, base, reps, R, K, stream, sh, binding):
                               w.context_lens[seqs], w.scale)
     rep = compare(out.cpu().numpy().view(np.uint16)[rows], ref)
     log(f"extend spot check on sequences {seqs}: {rep}")
+    del q_dev, qs_dev, out
     tflops = flops / (ms * 1e-3) / 1e12
     return {"workload": f"{w.name} batch, chunk = tokens after the shared prompt "
                         f"({int(chunk.min())}..{max_chunk}, {total} rows)",
@@ -446,110 +543,25 @@ def run_footprint(args):
 
 # ---------------------------------------------------------------- GPU timing
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=2)
-    ap.add_argument("--partition-size", type=int, default=None)
-    ap.add_argument("--replicas", type=int, default=None)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--hot", action=argparse.BooleanOptionalAction, default=True,
-                    help="also time steps on a single replica (cache-warm); --no-hot skips it")
-    ap.add_argument("--cascade", choices=["auto", "on", "off"], default="auto",
-                    help="shared-prefix cascade (auto: on when the batch shares a prefix)")
-    ap.add_argument("--prefix-partition-size", type=int, default=None,
-                    help="tokens per prefix partition (default: per workload, see DEFAULT_PREFIX_PARTITION)")
-    ap.add_argument("--schedule", choices=["on", "off"], default="on",
-                    help="run the decode over a host-built work list (non-empty items, longest first)")
-    ap.add_argument("--groups", choices=["auto", "on", "off"], default="auto",
-                    help="second level of sharing: groups of sequences (a fixer request's retries) "
-                         "that share tokens after the prefix (auto: when the workload has them)")
-    ap.add_argument("--graph", action="store_true",
-                    help="replay each step from a captured HIP graph (one per replica)")
-    ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
-    ap.add_argument("--ingest-stats", metavar="KERNEL_STATS_CSV")
-    ap.add_argument("--ingest-sq", nargs="+", metavar="COUNTER_CSV",
-                    help="write an SQ-counter summary (with --sq-kernel and --profile-name)")
-    ap.add_argument("--sq-kernel", default="cascade_kernel")
-    ap.add_argument("--command-note", default="")
-    ap.add_argument("--extend", action="store_true",
-                    help="also time extend (chunked prefill) attention: each sequence's tokens after "
-                         "its shared prompt as the chunk")
-    ap.add_argument("--footprint", action="store_true",
-                    help="isolated stage pools (shared prompt blocks) vs one engine holding private "
-                         "copies: KV blocks from the pool allocator and measured decode throughput, "
-                         "generator and fixer batches; prints its own JSON line")
-    ap.add_argument("--profile-name", default=None,
-                    help="file stem for --ingest-stats (default kernels_<workload>_stats)")
-    ap.add_argument("--profile-loop", type=int, default=0,
-                    help="only run this many decode launches (plus one calibration copy) and exit; "
-                         "for hardware-counter runs")
-    args = ap.parse_args()
-
-    if args.ingest_sq:
-        from workloads import CONFIG_NAMES
-        ingest_sq(args.ingest_sq, CONFIG_NAMES[args.config], args.sq_kernel, args.command_note,
-                  args.profile_name or f"sq_{CONFIG_NAMES[args.config]}")
-        return
-    if args.ingest_counters or args.ingest_stats:
-        from workloads import CONFIG_NAMES
-        name = CONFIG_NAMES[args.config]
-        if args.ingest_counters:
-            from workloads import build_config
-            wc = build_config(args.config, values=False)
-            plen = 0 if args.cascade == "off" else 16 * int(wc.meta.get("prefix_blocks", 0))
-            ingest_counters(*args.ingest_counters, name, decode_kernel_of(wc, plen), args.command_note)
-        if args.ingest_stats:
-            ingest_stats(args.ingest_stats, name, args.command_note, args.profile_name)
-        return
-
-    if args.footprint:
-        run_footprint(args)
-        return
-
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE={world}); "
-              "the decode-attention path runs on a single GPU", file=sys.stderr)
-        sys.exit(2)
-
-    from workloads import build_config, group_starts
-    t0 = time.perf_counter()
-    w = build_config(args.config)
-    w.partition_size = args.partition_size or DEFAULT_PARTITION.get(args.config, w.partition_size)
-    alg_bytes, logical_bytes = byte_accounting(w)
-    log(f"workload {w.name}: B={w.batch} Hq={w.num_q_heads} Hkv={w.num_kv_heads} D={w.head_dim} "
-        f"NB={w.num_blocks} max_ctx={w.max_context_len} alg={alg_bytes/1e6:.1f} MB "
-        f"logical={logical_bytes/1e6:.1f} MB (built in {time.perf_counter()-t0:.1f} s)")
-
-    cpu = None
-    if not args.no_cpu_baseline and not args.profile_loop:
-        log("cpu baseline (oracle) ...")
-        cpu = cpu_baseline(w, alg_bytes, args.cpu_seconds, logical_bytes)
-        log(f"cpu baseline: {cpu}")
-
+def measure(k, w, args, cpu, copy_gbps, headline, with_extend):
+    """Time one workload's decode steps in its launch configuration and return
+    its record (the headline fields, or one per_config entry)."""
     import torch
     from paper_2510_14126_amd import binding
     from paper_2510_14126_amd.device import PagedBatch
 
+    over = dict(partition_size=args.partition_size, prefix_partition_size=args.prefix_partition_size,
+                cascade=args.cascade, groups=args.groups) if headline else {}
+    S, kw = launch_configuration(k, w, **over)
+    w.partition_size = S
+    alg_bytes, logical_bytes = byte_accounting(w)
+    prefix_len = kw.get("prefix_len", 0)
+    group_len = kw.get("group_len", 0)
     dev = torch.device("cuda:0")
     pool_bytes = 2 * w.k_pool.nbytes
-    R = args.replicas or max(1, min(16, -(-(1 << 30) // pool_bytes)))
-    prefix_len = 16 * int(w.meta.get("prefix_blocks", 0))
-    if args.cascade == "off" or (args.cascade == "auto" and prefix_len == 0):
-        prefix_len = 0
-    pps = args.prefix_partition_size or default_prefix_partition(args.config, prefix_len)
-    group_len = 16 * int(w.meta.get("mid_blocks", 0)) if "groups" in w.meta else 0
-    if args.groups == "off" or (args.groups == "auto" and (group_len == 0 or prefix_len == 0)):
-        group_len = 0
-    if args.groups == "on" and group_len == 0:
-        raise SystemExit("--groups on: this workload has no groups sharing tokens after the prefix")
-    gkw = dict(group_start=group_starts(w), group_len=group_len) if group_len else {}
-    base = PagedBatch(w, dev, prefix_len=prefix_len, prefix_partition_size=pps,
-                      schedule=args.schedule == "on", **gkw)
+    R = (args.replicas if headline and args.replicas else
+         max(1, min(16, -(-(1 << 30) // pool_bytes))))
+    base = PagedBatch(w, dev, partition_size=S, schedule=args.schedule == "on", **kw)
     sched_host_us = None
     if base.items is not None:
         # host cost of the work list (a serving loop rebuilds it every step
@@ -564,68 +576,23 @@ def main():
     reps = [(base.pool, base.q)]
     keep = []
     for _ in range(1, R):
-        k, v, q = base.k.clone(), base.v.clone(), base.q.clone()
-        keep.append((k, v, q))
-        reps.append((binding.kv_pool_create(w.num_blocks, 16, w.num_kv_heads, w.head_dim, k, v), q))
+        kk, vv, qq = base.k.clone(), base.v.clone(), base.q.clone()
+        keep.append((kk, vv, qq))
+        reps.append((binding.kv_pool_create(w.num_blocks, 16, w.num_kv_heads, w.head_dim, kk, vv), qq))
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
     split = base.needs_reduce
 
-    def decode_on(i, s):
+    def decode_on(i, st):
         pool, q = reps[i % R]
-        if group_len:
-            n = 0 if base.items is None else int(base.items.numel())
-            binding.paged_attn_decode_cascade_groups(
-                pool, q, base.bt, base.bt_stride, base.ctx, base.batch, base.hq, w.scale,
-                base.max_ctx, base.partition_size, prefix_len, base.prefix_partition_size,
-                base.group_start, base.num_groups, base.max_group_size, group_len,
-                base.items if n else None, n, base.part_o, base.part_lse, s)
-            return
-        if base.items is not None:
-            n = int(base.items.numel())
-            if prefix_len:
-                binding.paged_attn_decode_cascade_scheduled(
-                    pool, q, base.bt, base.bt_stride, base.ctx, base.batch, base.hq, w.scale,
-                    base.max_ctx, base.partition_size, prefix_len, base.prefix_partition_size,
-                    base.items, n, base.part_o, base.part_lse, s)
-            else:
-                binding.paged_attn_decode_scheduled(
-                    pool, q, base.bt, base.bt_stride, base.ctx, base.batch, base.hq, w.scale,
-                    base.max_ctx, base.partition_size, base.items, n, base.out, base.part_o,
-                    base.part_lse, s)
-            return
-        if prefix_len:
-            binding.paged_attn_decode_cascade(pool, q, base.bt, base.bt_stride, base.ctx, base.batch,
-                                              base.hq, w.scale, base.max_ctx, base.partition_size,
-                                              prefix_len, base.prefix_partition_size, base.part_o,
-                                              base.part_lse, s)
-        else:
-            binding.paged_attn_decode(pool, q, base.bt, base.bt_stride, base.ctx, base.batch,
-                                      base.hq, w.scale, base.max_ctx, base.partition_size,
-                                      base.out, base.part_o, base.part_lse, s)
-
-    def reduce_on(s):
-        base.reduce(s)
+        base.decode(st, pool=pool, q=q)
 
     def decode(i):
         decode_on(i, sh)
 
     def reduce():
-        reduce_on(sh)
-
-    if args.profile_loop:
-        src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        binding.pa_stream_copy(src, dst, src.numel(), sh)      # calibration: 256 MiB each way
-        for i in range(args.profile_loop):
-            decode(i)
-            if split:
-                reduce()
-        torch.cuda.synchronize()
-        log(f"profile loop done: {args.profile_loop} decode launches, replicas={R}, "
-            f"calibration copy 268435456 bytes")
-        return
+        base.reduce(sh)
 
     for i in range(args.warmup):
         decode(i)
@@ -634,24 +601,25 @@ def main():
     torch.cuda.synchronize()
 
     K = args.steps
-    step_fn = [None] * R
-    if args.graph:
+    graphs = None
+    if args.graph and headline:
         # one captured step per replica; replays carry no host launch cost
+        graphs = []
         for r in range(R):
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
                 cs = torch.cuda.current_stream().cuda_stream
                 decode_on(r, cs)
                 if split:
-                    reduce_on(cs)
-            step_fn[r] = g
-        for r in range(R):
-            step_fn[r].replay()
+                    base.reduce(cs)
+            graphs.append(g)
+        for g in graphs:
+            g.replay()
         torch.cuda.synchronize()
 
     def step(i):
-        if args.graph:
-            step_fn[i % R].replay()
+        if graphs is not None:
+            graphs[i % R].replay()
         else:
             decode(i)
             if split:
@@ -672,18 +640,18 @@ def main():
 
     # per-kernel durations: K decode launches back to back between two events
     # on the launch stream, then K reduce launches the same way
-    e_dec = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
     torch.cuda.synchronize()
-    e_dec[0].record(stream)
+    ev[0].record(stream)
     for i in range(K):
         decode(i)
-    e_dec[1].record(stream)
+    ev[1].record(stream)
     for i in range(K if split else 0):
         reduce()
-    e_dec[2].record(stream)
+    ev[2].record(stream)
     torch.cuda.synchronize()
-    dec_avg = e_dec[0].elapsed_time(e_dec[1]) / K
-    red_avg = e_dec[1].elapsed_time(e_dec[2]) / K if split else 0.0
+    dec_avg = ev[0].elapsed_time(ev[1]) / K
+    red_avg = ev[1].elapsed_time(ev[2]) / K if split else 0.0
 
     # data-movement reference: the tiles the step reads (each distinct one
     # once), in the decode's grid shape, read with no arithmetic
@@ -701,44 +669,46 @@ def main():
             for i in range(3):
                 call(i)
             torch.cuda.synchronize()
-            e_dec[0].record(stream)
+            ev[0].record(stream)
             for i in range(K):
                 call(i)
-            e_dec[1].record(stream)
+            ev[1].record(stream)
             torch.cuda.synchronize()
-            us[nif] = 1e3 * e_dec[0].elapsed_time(e_dec[1]) / K
+            us[nif] = 1e3 * ev[0].elapsed_time(ev[1]) / K
         return us
 
     gather_us = time_gather(base.bt, base.bt_stride, base.batch, spans)
     best_nif = min(gather_us, key=gather_us.get)
     gather_avg = gather_us[best_nif] / 1e3
-    span_blocks = [(int(e) - (int(s) & ~15) + 15) // 16 for _, s, e in spans]
+    span_blocks = [(int(e) - (int(s0) & ~15) + 15) // 16 for _, s0, e in spans]
     tiles_read = int(sum(span_blocks)) * w.num_kv_heads
     gather_bytes = tiles_read * 2 * 16 * w.head_dim * 2
-    # the same spans with every span's blocks laid out contiguously (ids in
-    # order, one table row per span): the same bytes without fragmentation
-    crow = max(1, max(span_blocks, default=1))
-    ctab = np.zeros((max(1, n_spans), crow), dtype=np.int32)
-    nxt = 0
-    for i, nb in enumerate(span_blocks):
-        ctab[i, :nb] = np.arange(nxt, nxt + nb) % w.num_blocks
-        nxt += nb
-    cspans = np.stack([np.arange(n_spans), np.zeros(n_spans, np.int64),
-                       16 * np.asarray(span_blocks, np.int64)], axis=1) if n_spans else spans
-    contig_us = time_gather(torch.from_numpy(ctab).to(dev), crow, max(1, n_spans), cspans)
-    contig_avg = min(contig_us.values()) / 1e3
     gather_line = {"us_per_call": round(gather_avg * 1e3, 3), "kv_bytes": gather_bytes,
                    "tiles_in_flight": best_nif,
-                   "us_by_tiles_in_flight": {str(k): round(v, 3) for k, v in gather_us.items()},
+                   "us_by_tiles_in_flight": {str(a): round(b, 3) for a, b in gather_us.items()},
                    "gbps": round(gather_bytes / (gather_avg * 1e-3) / 1e9, 1),
                    "spans": n_spans,
-                   "decode_time_over_gather": round(dec_avg / gather_avg, 3),
-                   "contiguous_us_per_call": round(contig_avg * 1e3, 3),
-                   "contiguous_gbps": round(gather_bytes / (contig_avg * 1e-3) / 1e9, 1),
-                   "note": "pa_gather_tiles: the K/V tiles of this step (each once) read in the "
-                           "decode's grid shape with no arithmetic (the faster ring depth); "
-                           "contiguous: the same spans with each span's blocks stored in order"}
-    log(f"gather reference: {gather_line}")
+                   "decode_time_over_gather": round(dec_avg / gather_avg, 3)}
+    if headline:
+        # the same spans with every span's blocks laid out contiguously (ids in
+        # order, one table row per span): the same bytes without fragmentation
+        crow = max(1, max(span_blocks, default=1))
+        ctab = np.zeros((max(1, n_spans), crow), dtype=np.int32)
+        nxt = 0
+        for i, nb in enumerate(span_blocks):
+            ctab[i, :nb] = np.arange(nxt, nxt + nb) % w.num_blocks
+            nxt += nb
+        cspans = np.stack([np.arange(n_spans), np.zeros(n_spans, np.int64),
+                           16 * np.asarray(span_blocks, np.int64)], axis=1) if n_spans else spans
+        contig_us = time_gather(torch.from_numpy(ctab).to(dev), crow, max(1, n_spans), cspans)
+        contig_avg = min(contig_us.values()) / 1e3
+        gather_line.update({
+            "contiguous_us_per_call": round(contig_avg * 1e3, 3),
+            "contiguous_gbps": round(gather_bytes / (contig_avg * 1e-3) / 1e9, 1),
+            "note": "pa_gather_tiles: the K/V tiles of this step (each once) read in the "
+                    "decode's grid shape with no arithmetic (the faster ring depth); "
+                    "contiguous: the same spans with each span's blocks stored in order"})
+    log(f"[{w.name}] gather reference: {gather_line}")
 
     # hot: K steps back to back on one replica (its working set stays in the
     # caches), timed like the main loop
@@ -748,15 +718,14 @@ def main():
         if split:
             reduce()
         torch.cuda.synchronize()
-        e0 = torch.cuda.Event(enable_timing=True); e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
+        ev[0].record(stream)
         for i in range(K):
             decode(0)
             if split:
                 reduce()
-        e1.record(stream)
+        ev[1].record(stream)
         torch.cuda.synchronize()
-        hot_ms = e0.elapsed_time(e1) / K
+        hot_ms = ev[0].elapsed_time(ev[1]) / K
 
     # KV append of the step's new token, timed the same way.  The rows written
     # are the ones already stored at slot ctx-1, so the pools stay unchanged
@@ -766,46 +735,23 @@ def main():
     phys = w.block_tables[np.arange(w.batch), last // 16]
     k_new = torch.from_numpy(np.ascontiguousarray(w.k_pool[phys, :, last % 16, :]).view(np.int16)).to(dev)
     v_new = torch.from_numpy(np.ascontiguousarray(w.v_pool[phys, :, last % 16, :]).view(np.int16)).to(dev)
-    e_app = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     for i in range(3):
         binding.paged_attn_append_kv(reps[i % R][0], k_new, v_new, base.bt, base.bt_stride, base.ctx,
                                      base.batch, sh)
     torch.cuda.synchronize()
-    e_app[0].record(stream)
+    ev[0].record(stream)
     for i in range(K):
         binding.paged_attn_append_kv(reps[i % R][0], k_new, v_new, base.bt, base.bt_stride, base.ctx,
                                      base.batch, sh)
-    e_app[1].record(stream)
+    ev[1].record(stream)
     torch.cuda.synchronize()
-    app_ms = e_app[0].elapsed_time(e_app[1]) / K
+    app_ms = ev[0].elapsed_time(ev[1]) / K
     app_bytes = 4 * int(nz.sum()) * w.num_kv_heads * w.head_dim * 2      # K+V rows read and written
     append_line = {"us_per_call": round(app_ms * 1e3, 3), "bytes_per_call": app_bytes,
                    "gbps": round(app_bytes / (app_ms * 1e-3) / 1e9, 2),
                    "note": "one launch per step; launch-latency bound at these sizes"}
-    if cpu is not None:
-        from oracle import append_kv
-        kn_h, vn_h = w.k_pool[phys, :, last % 16, :], w.v_pool[phys, :, last % 16, :]
-        c0 = time.perf_counter()
-        append_kv(w.k_pool, w.v_pool, w.block_tables, w.context_lens, kn_h, vn_h)
-        cpu_s = time.perf_counter() - c0
-        append_line["cpu_oracle_us_per_call"] = round(cpu_s * 1e6, 1)
-        append_line["cpu_oracle_note"] = "numpy oracle, one call on one core (it copies both pools)"
 
-    extend_line = run_extend(w, base, reps, R, K, stream, sh, binding) if args.extend else None
-
-    # achievable copy bandwidth on this machine (read + write bytes)
-    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-    dst = torch.empty_like(src)
-    for _ in range(3):
-        binding.pa_stream_copy(src, dst, src.numel(), sh)
-    c0 = torch.cuda.Event(enable_timing=True); c1 = torch.cuda.Event(enable_timing=True)
-    c0.record(stream)
-    for _ in range(10):
-        binding.pa_stream_copy(src, dst, src.numel(), sh)
-    c1.record(stream)
-    torch.cuda.synchronize()
-    copy_gbps = 10 * 2 * src.numel() / (c0.elapsed_time(c1) * 1e-3) / 1e9
-    del src, dst
+    extend_line = run_extend(w, base, reps, R, K, stream, sh, binding) if with_extend else None
 
     # parity spot check of the benchmarked launch configuration
     from oracle import compare, decode_workload
@@ -815,29 +761,19 @@ def main():
     if split:
         reduce()
     torch.cuda.synchronize()
-    seqs = [0, int(np.argmax(w.context_lens)), w.batch - 1]
+    seqs = sorted({0, int(np.argmax(w.context_lens)), w.batch - 1})
     ref, _ = decode_workload(w, seqs=seqs)
     rep = compare(base.out_bits()[seqs], ref)
-    log(f"parity spot check on sequences {seqs}: {rep}")
+    log(f"[{w.name}] parity spot check on sequences {seqs}: {rep}")
 
     achieved = alg_bytes / (dec_avg * 1e-3) / 1e9
     value = alg_bytes / (ms_step * 1e-3) / 1e9
     kern = decode_kernel_of(w, prefix_len)
     traffic = traffic_from_profiles(w.name, kern)
-    line = {
-        "metric": "paged decode-attention KV GB/s (algorithmic bytes) and % of HBM peak; "
-                  "decode steps/s per batch",
+    rec = {
         "value": round(value, 2),
         "unit": "GB/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": args.warmup,
         "ms_per_step": round(ms_step, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded N(0,1) bf16 K/V/Q; stage-shaped block tables and lengths)",
         "config": {"workload": f"{w.name}: {w.meta['description']}", "batch": w.batch,
                    "num_q_heads": w.num_q_heads, "num_kv_heads": w.num_kv_heads,
                    "head_dim": w.head_dim, "block_size": 16, "partition_size": base.partition_size,
@@ -853,18 +789,19 @@ def main():
                    "work_list_host_us": sched_host_us,
                    "max_context_len": w.max_context_len, "parallelism": "single GPU"},
         "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
+        "frac_hbm_peak_step": round(value / HBM_PEAK_GBPS, 4),
+        "meets_70pct_hbm_target": bool(value >= 0.7 * HBM_PEAK_GBPS),
         "decode_steps_per_s": round(1000.0 / ms_step, 2),
         "tokens_per_s": round(w.batch * 1000.0 / ms_step, 1),
         "algorithmic_bytes_per_step": int(alg_bytes),
         "logical_kv_gbps_effective": round(logical_bytes / (ms_step * 1e-3) / 1e9, 2),
         "hot_ms_per_step": round(hot_ms, 5) if hot_ms is not None else None,
-        "launch": "hip graph replay per step" if args.graph else "direct launches",
+        "launch": "hip graph replay per step" if graphs is not None else "direct launches",
         "kernel_ms": {"decode_avg": round(dec_avg, 5), "reduce_avg": round(red_avg, 5)},
-        "copy_probe_gbps": round(copy_gbps, 1),
         "pct_of_copy_probe": round(100 * value / copy_gbps, 2),
         "wall_s_timed_region": round(wall, 4),
         "parity_spot_check": {"passed": rep.passed, "max_abs": rep.max_abs,
-                              "worst_row_rel_l2": rep.worst_row_rel_l2},
+                              "worst_row_rel_l2": rep.worst_row_rel_l2, "sequences": seqs},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic,
@@ -873,8 +810,229 @@ def main():
                      "bytes_per_launch": int(alg_bytes)},
         "gather_reference": gather_line,
         "append_kv": append_line,
-        "extend": extend_line,
         "cpu_baseline": cpu,
+    }
+    if extend_line is not None:
+        rec["extend"] = extend_line
+    # free this workload's device memory before the next one
+    for pool, _ in reps[1:]:
+        pool.close()
+    base.close()
+    del reps, keep, base, k_new, v_new, sink
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return rec
+
+
+def profile_loop(k, w, args):
+    """Only the decode launches (plus one calibration copy): for hardware-counter
+    and kernel-trace runs under rocprofv3.  With --stamp, first writes the
+    sources this run was built from."""
+    import torch
+    from paper_2510_14126_amd import binding
+    from paper_2510_14126_amd.device import PagedBatch
+    if args.stamp:
+        os.makedirs(os.path.dirname(os.path.abspath(args.stamp)), exist_ok=True)
+        with open(args.stamp, "w") as f:
+            json.dump(source_stamp(), f)
+    S, kw = launch_configuration(k, w, args.partition_size, args.prefix_partition_size,
+                                 args.cascade, args.groups)
+    dev = torch.device("cuda:0")
+    base = PagedBatch(w, dev, partition_size=S, schedule=args.schedule == "on", **kw)
+    pool_bytes = 2 * w.k_pool.nbytes
+    R = args.replicas or max(1, min(16, -(-(1 << 30) // pool_bytes)))
+    reps = [(base.pool, base.q)]
+    keep = []
+    for _ in range(1, R):
+        kk, vv, qq = base.k.clone(), base.v.clone(), base.q.clone()
+        keep.append((kk, vv, qq))
+        reps.append((binding.kv_pool_create(w.num_blocks, 16, w.num_kv_heads, w.head_dim, kk, vv), qq))
+    sh = torch.cuda.current_stream().cuda_stream
+    src = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    binding.pa_stream_copy(src, dst, src.numel(), sh)      # calibration: 256 MiB each way
+    if args.extend:
+        chunk, q_start, q = extend_inputs(w)
+        q_dev = torch.from_numpy(q.view(np.int16)).to(dev)
+        qs_dev = torch.from_numpy(q_start).to(dev)
+        out = torch.zeros_like(q_dev)
+        for i in range(args.profile_loop):
+            binding.paged_attn_extend(reps[i % R][0], q_dev, qs_dev, int(q_start[-1]), base.bt,
+                                      base.bt_stride, base.ctx, w.batch, w.num_q_heads, w.scale,
+                                      base.max_ctx, int(chunk.max()), out, sh)
+    else:
+        for i in range(args.profile_loop):
+            pool, q = reps[i % R]
+            base.decode(sh, pool=pool, q=q)
+            if base.needs_reduce:
+                base.reduce(sh)
+    torch.cuda.synchronize()
+    log(f"profile loop done: {args.profile_loop} {'extend' if args.extend else 'decode'} launches, "
+        f"replicas={R}, calibration copy 268435456 bytes")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=None,
+                    help="measure batch k alone (default: the long-context headline plus a "
+                         "per_config entry for each other batch)")
+    ap.add_argument("--partition-size", type=int, default=None)
+    ap.add_argument("--replicas", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="oracle time of the headline CPU baseline")
+    ap.add_argument("--cpu-seconds-per-config", type=float, default=3.0,
+                    help="oracle time of each per_config CPU baseline")
+    ap.add_argument("--hot", action=argparse.BooleanOptionalAction, default=True,
+                    help="also time steps on a single replica (cache-warm); --no-hot skips it")
+    ap.add_argument("--cascade", choices=["auto", "on", "off"], default="auto",
+                    help="shared-prefix cascade (auto: on when the batch shares a prefix)")
+    ap.add_argument("--prefix-partition-size", type=int, default=None,
+                    help="tokens per prefix partition (default: per workload, see DEFAULT_PREFIX_PARTITION)")
+    ap.add_argument("--schedule", choices=["on", "off"], default="on",
+                    help="run the decode over a host-built work list (non-empty items, longest first)")
+    ap.add_argument("--groups", choices=["auto", "on", "off"], default="auto",
+                    help="second level of sharing: groups of sequences (a fixer request's retries) "
+                         "that share tokens after the prefix (auto: when the workload has them)")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay each step from a captured HIP graph (one per replica)")
+    ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
+    ap.add_argument("--ingest-stats", metavar="KERNEL_STATS_CSV")
+    ap.add_argument("--ingest-sq", nargs="+", metavar="COUNTER_CSV",
+                    help="write an SQ-counter summary (with --sq-kernel and --profile-name)")
+    ap.add_argument("--sq-kernel", default="cascade_kernel")
+    ap.add_argument("--command-note", default="")
+    ap.add_argument("--stamp", default=None,
+                    help="--profile-loop: write the source stamp here; ingest: the stamp to check")
+    ap.add_argument("--extend", action="store_true",
+                    help="also time extend (chunked prefill) attention on --config k: each "
+                         "sequence's tokens after its shared prompt as the chunk (the default run "
+                         "times it on the fixer batch)")
+    ap.add_argument("--footprint", action="store_true",
+                    help="isolated stage pools vs one shared engine under a fixed KV budget; "
+                         "prints its own JSON line")
+    ap.add_argument("--profile-name", default=None,
+                    help="file stem for --ingest-stats (default kernels_<workload>_stats)")
+    ap.add_argument("--profile-loop", type=int, default=0,
+                    help="only run this many decode (or, with --extend, extend) launches of "
+                         "--config (default the headline batch) plus one calibration copy, and "
+                         "exit; for rocprofv3 runs")
+    args = ap.parse_args()
+
+    from workloads import CONFIG_NAMES, build_config
+    if args.ingest_sq or args.ingest_counters or args.ingest_stats:
+        k = args.config or HEADLINE_CONFIG
+        name = CONFIG_NAMES[k]
+        stamp = checked_stamp(args.stamp)
+        if args.ingest_sq:
+            ingest_sq(args.ingest_sq, name, args.sq_kernel, args.command_note,
+                      args.profile_name or f"sq_{name}", stamp)
+        if args.ingest_counters:
+            wc = build_config(k, values=False)
+            S, kw = launch_configuration(k, wc, args.partition_size, args.prefix_partition_size,
+                                         args.cascade, args.groups)
+            ingest_counters(*args.ingest_counters, name, decode_kernel_of(wc, kw.get("prefix_len", 0)),
+                            args.command_note, stamp)
+        if args.ingest_stats:
+            ingest_stats(args.ingest_stats, name, args.command_note, stamp, args.profile_name)
+        return
+
+    if args.footprint:
+        run_footprint(args)
+        return
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE={world}); "
+              "the decode-attention path runs on a single GPU", file=sys.stderr)
+        sys.exit(2)
+
+    head_k = args.config or HEADLINE_CONFIG
+    extra = [] if args.config or args.profile_loop else [c for c in PER_CONFIG if c != head_k]
+    t0 = time.perf_counter()
+    ws = {}
+    for k in [head_k] + extra:
+        ws[k] = build_config(k)
+        S, _ = launch_configuration(k, ws[k])
+        ws[k].partition_size = S
+        alg, logical = byte_accounting(ws[k])
+        log(f"workload {ws[k].name}: B={ws[k].batch} Hq={ws[k].num_q_heads} Hkv={ws[k].num_kv_heads} "
+            f"D={ws[k].head_dim} NB={ws[k].num_blocks} max_ctx={ws[k].max_context_len} "
+            f"alg={alg/1e6:.1f} MB logical={logical/1e6:.1f} MB ({time.perf_counter()-t0:.1f} s)")
+
+    if args.profile_loop:
+        profile_loop(head_k, ws[head_k], args)
+        return
+
+    # CPU baselines first: the oracle's worker pools are forked before the
+    # process touches the GPU
+    cpu = {}
+    if not args.no_cpu_baseline:
+        for k in [head_k] + extra:
+            alg, logical = byte_accounting(ws[k])
+            secs = args.cpu_seconds if k == head_k else args.cpu_seconds_per_config
+            log(f"cpu baseline (oracle) {ws[k].name} ...")
+            cpu[k] = cpu_baseline(ws[k], alg, secs, logical)
+            log(f"cpu baseline {ws[k].name}: {cpu[k]}")
+
+    import torch
+    from paper_2510_14126_amd import binding
+    dev = torch.device("cuda:0")
+    sh = torch.cuda.current_stream().cuda_stream
+    # achievable copy bandwidth on this box (read + write bytes)
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        binding.pa_stream_copy(src, dst, src.numel(), sh)
+    c0 = torch.cuda.Event(enable_timing=True); c1 = torch.cuda.Event(enable_timing=True)
+    c0.record()
+    for _ in range(10):
+        binding.pa_stream_copy(src, dst, src.numel(), sh)
+    c1.record()
+    torch.cuda.synchronize()
+    copy_gbps = 10 * 2 * src.numel() / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+
+    head = measure(head_k, ws.pop(head_k), args, cpu.get(head_k), copy_gbps, True,
+                   args.extend)
+    per_config = []
+    extend_line = head.pop("extend", None)
+    for k in extra:
+        w = ws.pop(k)
+        rec = measure(k, w, args, cpu.get(k), copy_gbps, False, with_extend=(k == 3))
+        if "extend" in rec:
+            extend_line = rec.pop("extend")
+        rec = {"config_index": k, "workload": w.name, **rec}
+        per_config.append(rec)
+        log(f"per_config {w.name}: {rec['ms_per_step']} ms/step, {rec['value']} GB/s "
+            f"({rec['pct_hbm_peak']}% of peak), decode {rec['kernel_ms']['decode_avg']} ms, "
+            f"parity {rec['parity_spot_check']['passed']}")
+        del w
+
+    line = {
+        "metric": "paged decode-attention KV GB/s (algorithmic bytes) and % of HBM peak; "
+                  "decode steps/s per batch",
+        "value": head["value"],
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 K/V/Q; stage-shaped block tables and lengths)",
+        **{k: v for k, v in head.items() if k not in ("value", "unit", "ms_per_step")},
+        "copy_probe_gbps": round(copy_gbps, 1),
+        "per_config": per_config,
+        "target_70pct_hbm_on_configs_1_to_4": (
+            {r["workload"]: r["meets_70pct_hbm_target"] for r in per_config} if per_config else None),
+        "extend": extend_line,
     }
     print(json.dumps(line), flush=True)
 

@@ -146,7 +146,9 @@ int paged_attn_workspace_size(int32_t batch, int32_t num_q_heads, int32_t head_d
  *   pool             geometry and K/V device pointers (kv_pool_create)
  *   q                device bf16 [batch][num_q_heads][head_dim], 16-byte aligned
  *   block_tables     device int32 [batch][bt_stride]; entries 0..ceil(ctx/16)-1
- *                    of row b are physical ids, later entries are never read
+ *                    of row b are physical ids.  The kernels may load later
+ *                    entries of the row (within bt_stride) before the length
+ *                    arrives, but never use them: they may hold anything
  *   bt_stride        >= ceil(max_context_len / 16)
  *   context_lens     device int32 [batch]: tokens to attend (the current token
  *                    included); 0 gives a zero output row
@@ -210,8 +212,8 @@ int paged_attn_cascade_workspace_size(int32_t batch, int32_t num_q_heads, int32_
  * partitions and of the per-sequence partitions after the prefix into
  * partial_out / partial_lse (sizes from paged_attn_cascade_workspace_size).
  * The caller guarantees that entries 0 .. prefix_len/16 - 1 of every block
- * table row are the same physical blocks; the prefix pass reads them from
- * row 0.  A sequence shorter than prefix_len attends only to its own
+ * table row are the same physical blocks (paged_attn_check_tables verifies
+ * it on host copies); the prefix pass reads them from row 0.  A sequence shorter than prefix_len attends only to its own
  * context.  The prefix pass needs head_dim 128; other arguments as in
  * paged_attn_decode.  Follow with paged_attn_reduce_cascade on the same
  * stream. */
@@ -364,6 +366,87 @@ int paged_attn_decode_cascade_scheduled(const pa_kv_pool *pool, const void *q,
                                         int32_t prefix_partition_size, const int32_t *items,
                                         int32_t num_items, float *partial_out,
                                         float *partial_lse, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Index traces of the launches that take a shared prefix, groups or a work
+ * list, and a host-side check of the sharing they rely on.
+ *
+ * Block-table and context-length handling must be exact: every tile a
+ * launch reads is named by a table entry and bounded by a context length.
+ * The trace variants run the same gather code as their production entry
+ * points and also record, for every work item, the ordered list of KV tiles
+ * it loaded as int32 triples (logical block j, physical id as read from the
+ * table, valid rows).  The stage pools share prompt blocks between
+ * sequences (Cortex paper, section 1; section 2, "Cortex Benefits"); the
+ * cascade reads those shared entries from one row only, so a caller that
+ * holds its tables on the host can verify that they really are shared.
+ * ------------------------------------------------------------------------- */
+
+/* paged_attn_decode_scheduled with the index trace of paged_attn_decode_trace
+ * (same layout: work item (partition p, sequence b, KV head g) at
+ * ((p * batch + b) * num_kv_heads + g) * trace_tiles triples). */
+int paged_attn_decode_scheduled_trace(const pa_kv_pool *pool, const void *q,
+                                      const int32_t *block_tables, int32_t bt_stride,
+                                      const int32_t *context_lens, int32_t batch,
+                                      int32_t num_q_heads, float scale, int32_t max_context_len,
+                                      int32_t partition_size, const int32_t *items,
+                                      int32_t num_items, void *out, float *partial_out,
+                                      float *partial_lse, int32_t *trace, int64_t trace_capacity,
+                                      void *stream);
+
+/* Layout of a cascade step's index trace, in int32 values (three per tile):
+ *   layout_out[0], [1]  offset and tiles per item of the prefix partitions:
+ *                       partition p, row group r (64 query rows of one KV
+ *                       head, r = 0 .. ceil(batch*G/64)-1), KV head g at
+ *                       offset + ((p * row_groups + r) * num_kv_heads + g)
+ *                       * tiles * 3; slot i is block i of the partition
+ *   layout_out[2], [3]  the same for the groups: group k, KV head g at
+ *                       offset + (k * num_kv_heads + g) * tiles * 3
+ *   layout_out[4], [5]  the per-sequence partitions after the shared tokens:
+ *                       (partition p, sequence b, KV head g) at offset +
+ *                       ((p * batch + b) * num_kv_heads + g) * tiles * 3
+ *   layout_out[6]       total int32 values
+ * Arguments as in paged_attn_decode_cascade_groups (group_len 0: no groups). */
+int paged_attn_cascade_trace_layout(const pa_kv_pool *pool, int32_t batch, int32_t num_q_heads,
+                                    int32_t max_context_len, int32_t partition_size,
+                                    int32_t prefix_len, int32_t prefix_partition_size,
+                                    int32_t num_groups, int32_t group_len, int64_t layout_out[7]);
+
+/* The cascade decode (plain: group_len 0 and group_start NULL; grouped:
+ * group_len > 0; over a work list: items non-NULL, else the full grid) with
+ * its index trace in the layout above; entries of items that load no tile
+ * are left untouched.  Every shared-span workgroup records the tiles of its
+ * span (all of its row groups read the same ones).  trace_capacity: int32
+ * values the buffer holds (PA_EINVAL if fewer than layout_out[6]).  Other
+ * arguments and the partials as in paged_attn_decode_cascade_groups. */
+int paged_attn_decode_cascade_trace(const pa_kv_pool *pool, const void *q,
+                                    const int32_t *block_tables, int32_t bt_stride,
+                                    const int32_t *context_lens, int32_t batch,
+                                    int32_t num_q_heads, float scale, int32_t max_context_len,
+                                    int32_t partition_size, int32_t prefix_len,
+                                    int32_t prefix_partition_size, const int32_t *group_start,
+                                    int32_t num_groups, int32_t max_group_size, int32_t group_len,
+                                    const int32_t *items, int32_t num_items, float *partial_out,
+                                    float *partial_lse, int32_t *trace, int64_t trace_capacity,
+                                    void *stream);
+
+/* Host-side check of block tables before a launch (HOST pointers; nothing
+ * runs on the GPU):
+ *   - every context length is in [0, 16 * bt_stride] and every entry that
+ *     a sequence's own context uses names a block of the pool;
+ *   - prefix_len > 0: for every sequence b, the entries the cascade's
+ *     prefix pass reads for it through row 0 (blocks 0 .. ceil(min(ctx_b,
+ *     prefix_len) / 16) - 1) equal row b's own;
+ *   - group_len > 0: group_start [num_groups + 1] runs nondecreasing from 0
+ *     to batch, and every member b of group k has the entries the group pass
+ *     reads for it through the group's first row (blocks prefix_len/16 ..
+ *     ceil(min(ctx_b, prefix_len + group_len) / 16) - 1) in its own row.
+ * Returns PA_OK, or PA_EINVAL with a message naming the sequence, entry and
+ * values; *bad_seq_out (may be NULL) receives the failing sequence, or -1. */
+int paged_attn_check_tables(const pa_kv_pool *pool, const int32_t *block_tables, int32_t bt_stride,
+                            const int32_t *context_lens, int32_t batch, int32_t prefix_len,
+                            const int32_t *group_start, int32_t num_groups, int32_t group_len,
+                            int32_t *bad_seq_out);
 
 /* ---------------------------------------------------------------------------
  * KV append.

@@ -63,6 +63,15 @@ SIGNATURES = {
                                                      _i32, _i32, _i32, _vp, _i32, _vp, _vp, _vp]),
     "paged_attn_extend": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _vp, _i32, _i32, _f32, _i32, _i32,
                                    _vp, _vp]),
+    "paged_attn_decode_scheduled_trace": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32,
+                                                   _i32, _vp, _i32, _vp, _vp, _vp, _vp, _i64, _vp]),
+    "paged_attn_cascade_trace_layout": (_c_int, [_vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32,
+                                                 _pi64]),
+    "paged_attn_decode_cascade_trace": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32,
+                                                 _i32, _i32, _i32, _vp, _i32, _i32, _i32, _vp, _i32,
+                                                 _vp, _vp, _vp, _i64, _vp]),
+    "paged_attn_check_tables": (_c_int, [_vp, _pi32, _i32, _pi32, _i32, _i32, _pi32, _i32, _i32,
+                                         _pi32]),
     "paged_attn_cascade_workspace_size": (_c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _i32,
                                                    ctypes.POINTER(_sz), ctypes.POINTER(_sz),
                                                    _pi32]),
@@ -373,3 +382,58 @@ def paged_attn_decode_cascade_scheduled(pool: KVPool, q, block_tables, bt_stride
         pool._handle(), _ptr(q), _ptr(block_tables), bt_stride, _ptr(context_lens), batch,
         num_q_heads, scale, max_context_len, partition_size, prefix_len, prefix_partition_size,
         _ptr(items), num_items, _ptr(partial_out), _ptr(partial_lse), _ptr(stream)))
+
+
+def paged_attn_decode_scheduled_trace(pool: KVPool, q, block_tables, bt_stride, context_lens, batch,
+                                      num_q_heads, scale, max_context_len, partition_size, items,
+                                      num_items, out, partial_out, partial_lse, trace,
+                                      trace_capacity, stream=None) -> None:
+    _check(_lib.paged_attn_decode_scheduled_trace(
+        pool._handle(), _ptr(q), _ptr(block_tables), bt_stride, _ptr(context_lens), batch,
+        num_q_heads, scale, max_context_len, partition_size, _ptr(items), num_items, _ptr(out),
+        _ptr(partial_out), _ptr(partial_lse), _ptr(trace), trace_capacity, _ptr(stream)))
+
+
+def paged_attn_cascade_trace_layout(pool: KVPool, batch, num_q_heads, max_context_len,
+                                    partition_size, prefix_len, prefix_partition_size,
+                                    num_groups=0, group_len=0) -> dict:
+    """Offsets (int32 values) and tiles per item of the trace sections."""
+    lay = (ctypes.c_int64 * 7)()
+    _check(_lib.paged_attn_cascade_trace_layout(pool._handle(), batch, num_q_heads, max_context_len,
+                                                partition_size, prefix_len, prefix_partition_size,
+                                                num_groups, group_len, lay))
+    keys = ("prefix_offset", "prefix_tiles", "group_offset", "group_tiles", "decode_offset",
+            "decode_tiles", "total")
+    return dict(zip(keys, [int(x) for x in lay]))
+
+
+def paged_attn_decode_cascade_trace(pool: KVPool, q, block_tables, bt_stride, context_lens, batch,
+                                    num_q_heads, scale, max_context_len, partition_size, prefix_len,
+                                    prefix_partition_size, group_start, num_groups, max_group_size,
+                                    group_len, items, num_items, partial_out, partial_lse, trace,
+                                    trace_capacity, stream=None) -> None:
+    _check(_lib.paged_attn_decode_cascade_trace(
+        pool._handle(), _ptr(q), _ptr(block_tables), bt_stride, _ptr(context_lens), batch,
+        num_q_heads, scale, max_context_len, partition_size, prefix_len, prefix_partition_size,
+        _ptr(group_start), num_groups, max_group_size, group_len, _ptr(items), num_items,
+        _ptr(partial_out), _ptr(partial_lse), _ptr(trace), trace_capacity, _ptr(stream)))
+
+
+def paged_attn_check_tables(pool: KVPool, block_tables, context_lens, prefix_len=0,
+                            group_start=None, group_len=0) -> None:
+    """Host-side check of numpy block tables and lengths (raises PagedAttnError
+    with the failing sequence in ``.bad_seq``)."""
+    import numpy as np
+    bt = np.ascontiguousarray(np.asarray(block_tables, dtype=np.int32))
+    ctx = np.ascontiguousarray(np.asarray(context_lens, dtype=np.int32))
+    gs = None if group_start is None else np.ascontiguousarray(np.asarray(group_start, dtype=np.int32))
+    bad = ctypes.c_int32(-1)
+    rc = _lib.paged_attn_check_tables(
+        pool._handle(), bt.ctypes.data_as(_pi32), int(bt.shape[1]) if bt.ndim == 2 else 1,
+        ctx.ctypes.data_as(_pi32), int(ctx.size), prefix_len,
+        gs.ctypes.data_as(_pi32) if gs is not None else None,
+        int(gs.size - 1) if gs is not None else 0, group_len, ctypes.byref(bad))
+    if rc != PA_OK:
+        err = PagedAttnError(rc, _lib.pa_last_error().decode())
+        err.bad_seq = bad.value
+        raise err

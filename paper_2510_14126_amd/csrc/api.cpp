@@ -23,9 +23,11 @@ struct pa_kv_pool {
 };
 
 namespace {
-
 thread_local std::string g_err = "no error";
+}  // namespace
 
+namespace pa {
+// Records the message that pa_last_error() returns and passes the code on.
 int fail(int code, const char* fmt, ...) {
   char buf[512];
   va_list ap;
@@ -35,6 +37,10 @@ int fail(int code, const char* fmt, ...) {
   g_err = buf;
   return code;
 }
+}  // namespace pa
+
+namespace {
+using pa::fail;
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -257,6 +263,29 @@ int plan_cascade(int32_t max_context_len, int32_t partition_size, int32_t prefix
   const int64_t stride = (int64_t)out->pre_parts + out->group_parts + out->suf_parts;
   out->stride = (int32_t)(stride > 0 ? stride : 1);
   return PA_OK;
+}
+
+// Where the index trace of a cascade step puts each kind of work item, in
+// int32 values (three per tile): the prefix partitions' tiles, then the
+// groups', then the per-sequence partitions'.
+struct TraceLayout {
+  int64_t prefix_offset, prefix_tiles;
+  int64_t group_offset, group_tiles;
+  int64_t decode_offset, decode_tiles;
+  int64_t total;
+};
+
+void cascade_trace_layout(int32_t num_kv_heads, int32_t batch, int32_t group, const CascadePlan& cp,
+                          int32_t num_groups, int32_t group_len, TraceLayout* t) {
+  const int64_t row_groups = ((int64_t)batch * group + pa::kSharedRowsPerWg - 1) / pa::kSharedRowsPerWg;
+  t->prefix_tiles = cp.pre_tokens / PA_BLOCK_SIZE;
+  t->group_tiles = group_len / PA_BLOCK_SIZE;
+  t->decode_tiles = cp.suf_tokens / PA_BLOCK_SIZE;
+  t->prefix_offset = 0;
+  t->group_offset = t->prefix_offset + 3 * (int64_t)cp.pre_parts * row_groups * num_kv_heads * t->prefix_tiles;
+  const int64_t groups = group_len > 0 ? num_groups : 0;
+  t->decode_offset = t->group_offset + 3 * groups * num_kv_heads * t->group_tiles;
+  t->total = t->decode_offset + 3 * (int64_t)cp.suf_parts * batch * num_kv_heads * t->decode_tiles;
 }
 
 }  // namespace
@@ -487,7 +516,8 @@ int cascade_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tab
                  float* partial_out, float* partial_lse, void* stream, const char* fn,
                  bool scheduled, const int32_t* items, int32_t num_items,
                  const int32_t* group_start = nullptr, int32_t num_groups = 0,
-                 int32_t max_group_size = 0, int32_t group_len = 0) {
+                 int32_t max_group_size = 0, int32_t group_len = 0, int32_t* trace = nullptr,
+                 int64_t trace_capacity = 0, bool tracing = false) {
   const DecodeArgs a{pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
                      max_context_len};
   int32_t group = 0;
@@ -520,6 +550,14 @@ int cascade_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tab
     rc = validate_items(items, num_items, (int64_t)cp.suf_parts * batch, fn);
     if (rc) return rc;
   }
+  TraceLayout tl;
+  if (tracing) {
+    cascade_trace_layout(pool->num_kv_heads, batch, group, cp, num_groups, group_len, &tl);
+    if (!trace || !aligned(trace, 4)) return fail(PA_EINVAL, "%s: trace buffer is NULL or misaligned", fn);
+    if (trace_capacity < tl.total)
+      return fail(PA_EINVAL, "%s: trace_capacity %lld < %lld int32 values", fn,
+                  (long long)trace_capacity, (long long)tl.total);
+  }
   if (batch == 0) return PA_OK;
   if (!partial_out || !partial_lse) return fail(PA_EINVAL, "%s: partial buffers are NULL", fn);
   if (!aligned(partial_out, 16) || !aligned(partial_lse, 4))
@@ -550,6 +588,12 @@ int cascade_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tab
     pp.group_len = group_len;
   }
   pp.scale_log2 = scale * 1.4426950408889634f;
+  if (tracing) {
+    pp.trace_prefix = trace + tl.prefix_offset;
+    pp.trace_group = trace + tl.group_offset;
+    pp.prefix_trace_tiles = tl.prefix_tiles;
+    pp.group_trace_tiles = tl.group_tiles;
+  }
   pa::DecodeParams p = decode_params(a);
   p.part_o = partial_out;
   p.part_lse = partial_lse;
@@ -561,18 +605,19 @@ int cascade_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tab
   p.part_stride = cp.stride;
   p.write_partials = 1;
   p.trace_tiles = cp.suf_tokens / PA_BLOCK_SIZE;
+  if (tracing) p.trace = trace + tl.decode_offset;
   if (scheduled) {
     p.items = items;
     p.num_items = num_items;
   }
   if (pool->head_dim == 128) {
     // prefix pass and per-sequence decode in one grid
-    hipError_t e = pa::launch_cascade(pp, p, group, st);
+    hipError_t e = pa::launch_cascade(pp, p, group, tracing, st);
     if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
     return PA_OK;
   }
   if (cp.suf_parts > 0) {  // no shared pass (head_dim 64 requires prefix_len 0, no groups)
-    hipError_t e = launch_decode(p, pool, group, false, stream);
+    hipError_t e = launch_decode(p, pool, group, tracing, stream);
     if (e != hipSuccess) return fail(PA_EHIP, "%s: kernel launch failed: %s", fn, hipGetErrorString(e));
   }
   return PA_OK;
@@ -637,6 +682,136 @@ int paged_attn_decode_scheduled(const pa_kv_pool* pool, const void* q, const int
                      max_context_len};
   return decode_impl(a, partition_size, out, partial_out, partial_lse, nullptr, 0, false, stream,
                      "paged_attn_decode_scheduled", true, items, num_items);
+}
+
+int paged_attn_decode_scheduled_trace(const pa_kv_pool* pool, const void* q,
+                                      const int32_t* block_tables, int32_t bt_stride,
+                                      const int32_t* context_lens, int32_t batch, int32_t num_q_heads,
+                                      float scale, int32_t max_context_len, int32_t partition_size,
+                                      const int32_t* items, int32_t num_items, void* out,
+                                      float* partial_out, float* partial_lse, int32_t* trace,
+                                      int64_t trace_capacity, void* stream) {
+  const DecodeArgs a{pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
+                     max_context_len};
+  return decode_impl(a, partition_size, out, partial_out, partial_lse, trace, trace_capacity, true,
+                     stream, "paged_attn_decode_scheduled_trace", true, items, num_items);
+}
+
+int paged_attn_cascade_trace_layout(const pa_kv_pool* pool, int32_t batch, int32_t num_q_heads,
+                                    int32_t max_context_len, int32_t partition_size,
+                                    int32_t prefix_len, int32_t prefix_partition_size,
+                                    int32_t num_groups, int32_t group_len, int64_t layout_out[7]) {
+  const char* fn = "paged_attn_cascade_trace_layout";
+  if (!pool || !layout_out) return fail(PA_EINVAL, "%s: NULL argument", fn);
+  if (batch < 0) return fail(PA_EINVAL, "%s: batch = %d < 0", fn, batch);
+  if (num_q_heads <= 0 || num_q_heads % pool->num_kv_heads != 0)
+    return fail(PA_EINVAL, "%s: num_q_heads = %d is not a positive multiple of num_kv_heads = %d", fn,
+                num_q_heads, pool->num_kv_heads);
+  if (group_len > 0 && (num_groups < 1 || num_groups > batch))
+    return fail(PA_EINVAL, "%s: num_groups = %d outside [1, batch]", fn, num_groups);
+  CascadePlan cp;
+  const int rc = plan_cascade(max_context_len, partition_size, prefix_len, prefix_partition_size,
+                              group_len, &cp, fn);
+  if (rc) return rc;
+  TraceLayout t;
+  cascade_trace_layout(pool->num_kv_heads, batch, num_q_heads / pool->num_kv_heads, cp, num_groups,
+                       group_len, &t);
+  const int64_t v[7] = {t.prefix_offset, t.prefix_tiles, t.group_offset, t.group_tiles,
+                        t.decode_offset, t.decode_tiles, t.total};
+  for (int i = 0; i < 7; ++i) layout_out[i] = v[i];
+  return PA_OK;
+}
+
+int paged_attn_decode_cascade_trace(const pa_kv_pool* pool, const void* q,
+                                    const int32_t* block_tables, int32_t bt_stride,
+                                    const int32_t* context_lens, int32_t batch, int32_t num_q_heads,
+                                    float scale, int32_t max_context_len, int32_t partition_size,
+                                    int32_t prefix_len, int32_t prefix_partition_size,
+                                    const int32_t* group_start, int32_t num_groups,
+                                    int32_t max_group_size, int32_t group_len, const int32_t* items,
+                                    int32_t num_items, float* partial_out, float* partial_lse,
+                                    int32_t* trace, int64_t trace_capacity, void* stream) {
+  const char* fn = "paged_attn_decode_cascade_trace";
+  if (group_len < 0) return fail(PA_EINVAL, "%s: group_len = %d < 0", fn, group_len);
+  return cascade_impl(pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
+                      max_context_len, partition_size, prefix_len, prefix_partition_size,
+                      partial_out, partial_lse, stream, fn, items != nullptr, items, num_items,
+                      group_len > 0 ? group_start : nullptr, group_len > 0 ? num_groups : 0,
+                      max_group_size, group_len, trace, trace_capacity, true);
+}
+
+int paged_attn_check_tables(const pa_kv_pool* pool, const int32_t* block_tables, int32_t bt_stride,
+                            const int32_t* context_lens, int32_t batch, int32_t prefix_len,
+                            const int32_t* group_start, int32_t num_groups, int32_t group_len,
+                            int32_t* bad_seq_out) {
+  const char* fn = "paged_attn_check_tables";
+  if (bad_seq_out) *bad_seq_out = -1;
+  if (!pool) return fail(PA_EINVAL, "%s: pool is NULL", fn);
+  if (batch < 0) return fail(PA_EINVAL, "%s: batch = %d < 0", fn, batch);
+  if (bt_stride < 1 || (int64_t)bt_stride * PA_BLOCK_SIZE > 0x7fffffffLL)
+    return fail(PA_EINVAL, "%s: bt_stride = %d outside [1, 2^27)", fn, bt_stride);
+  if (prefix_len < 0 || prefix_len % PA_BLOCK_SIZE != 0)
+    return fail(PA_EINVAL, "%s: prefix_len = %d is not a non-negative multiple of %d", fn, prefix_len,
+                PA_BLOCK_SIZE);
+  if (group_len < 0 || group_len % PA_BLOCK_SIZE != 0)
+    return fail(PA_EINVAL, "%s: group_len = %d is not a non-negative multiple of %d", fn, group_len,
+                PA_BLOCK_SIZE);
+  if (batch == 0) return PA_OK;
+  if (!block_tables || !context_lens) return fail(PA_EINVAL, "%s: NULL table or lengths", fn);
+  auto bad = [&](int32_t b) {
+    if (bad_seq_out) *bad_seq_out = b;
+    return PA_EINVAL;
+  };
+  const int64_t cap = (int64_t)bt_stride * PA_BLOCK_SIZE;
+  // every entry a sequence's own context uses is a block of the pool
+  for (int32_t b = 0; b < batch; ++b) {
+    const int64_t n = context_lens[b];
+    if (n < 0 || n > cap) {
+      fail(PA_EINVAL, "%s: context_lens[%d] = %lld outside [0, 16 * bt_stride = %lld]", fn, b,
+           (long long)n, (long long)cap);
+      return bad(b);
+    }
+    const int32_t* row = block_tables + (size_t)b * bt_stride;
+    for (int64_t j = 0; j < (n + PA_BLOCK_SIZE - 1) / PA_BLOCK_SIZE; ++j)
+      if (row[j] < 0 || row[j] >= pool->num_blocks) {
+        fail(PA_EINVAL, "%s: block_tables[%d][%lld] = %d is not a block of the pool (0 .. %d)", fn, b,
+             (long long)j, row[j], pool->num_blocks - 1);
+        return bad(b);
+      }
+  }
+  // Sequence b's tokens t < min(ctx_b, end) of a shared span [begin, end)
+  // are read through row `owner` instead of row b: those entries must match.
+  auto shared = [&](int32_t b, int32_t owner, int64_t begin, int64_t end, const char* what) {
+    const int64_t n = std::min<int64_t>(context_lens[b], end);
+    const int32_t* row = block_tables + (size_t)b * bt_stride;
+    const int32_t* own = block_tables + (size_t)owner * bt_stride;
+    for (int64_t j = begin / PA_BLOCK_SIZE; j < (n + PA_BLOCK_SIZE - 1) / PA_BLOCK_SIZE; ++j)
+      if (row[j] != own[j]) {
+        fail(PA_EINVAL, "%s: block_tables[%d][%lld] = %d differs from %s block %d in row %d", fn, b,
+             (long long)j, row[j], what, own[j], owner);
+        return false;
+      }
+    return true;
+  };
+  if (prefix_len > 0) {
+    if (prefix_len > cap) return fail(PA_EINVAL, "%s: prefix_len exceeds the table", fn);
+    for (int32_t b = 1; b < batch; ++b)
+      if (!shared(b, 0, 0, prefix_len, "the shared-prefix")) return bad(b);
+  }
+  if (group_len > 0) {
+    if ((int64_t)prefix_len + group_len > cap) return fail(PA_EINVAL, "%s: prefix_len + group_len exceeds the table", fn);
+    if (!group_start || num_groups < 1 || num_groups > batch)
+      return fail(PA_EINVAL, "%s: group_start is NULL or num_groups = %d outside [1, batch]", fn, num_groups);
+    if (group_start[0] != 0 || group_start[num_groups] != batch)
+      return fail(PA_EINVAL, "%s: group_start must run from 0 to batch = %d", fn, batch);
+    for (int32_t k = 0; k < num_groups; ++k) {
+      const int32_t s0 = group_start[k], s1 = group_start[k + 1];
+      if (s1 < s0) return fail(PA_EINVAL, "%s: group_start decreases at group %d", fn, k);
+      for (int32_t b = s0 + 1; b < s1; ++b)
+        if (!shared(b, s0, prefix_len, (int64_t)prefix_len + group_len, "its group's")) return bad(b);
+    }
+  }
+  return PA_OK;
 }
 
 int paged_attn_schedule(const int32_t* context_lens, int32_t batch, int32_t max_context_len,

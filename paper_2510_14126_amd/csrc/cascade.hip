@@ -26,7 +26,7 @@ static_assert(PA_VALU_WAVES == mfma::kWaves, "both halves use the same workgroup
 // than the 3-deep ring of the standalone kernel.
 constexpr int kCascadeValuNbuf = 2;
 
-template <int G>
+template <int G, bool TRACE>
 __global__ void __launch_bounds__(64 * mfma::kWaves) __attribute__((amdgpu_waves_per_eu(2, 8)))
 cascade_kernel(const PrefixParams pp, const DecodeParams dp, int prefix_runs, int group_runs,
                int decode_runs) {
@@ -65,22 +65,22 @@ cascade_kernel(const PrefixParams pp, const DecodeParams dp, int prefix_runs, in
   }
   if (shared) {
     if (idx < prefix_runs)
-      mfma::prefix_mfma_body<G>(pp, idx * hkv + g, lds);
+      mfma::prefix_mfma_body<G, TRACE>(pp, idx * hkv + g, lds);
     else
-      mfma::group_mfma_body<G>(pp, (idx - prefix_runs) * hkv + g, lds);
+      mfma::group_mfma_body<G, TRACE>(pp, (idx - prefix_runs) * hkv + g, lds);
     return;
   }
   const int wg = idx * hkv + g;
   if constexpr (G == 4) {
-    valu::decode_valu_body<128, 4, PA_VALU_WAVES, kCascadeValuNbuf, false>(dp, wg, lds);
+    valu::decode_valu_body<128, 4, PA_VALU_WAVES, kCascadeValuNbuf, TRACE>(dp, wg, lds);
   } else {
-    mfma::decode_mfma_body<false>(dp, wg, lds);
+    mfma::decode_mfma_body<TRACE>(dp, wg, lds);
   }
 }
 
 }  // namespace
 
-hipError_t launch_cascade(const PrefixParams& pp, const DecodeParams& dp, int group,
+hipError_t launch_cascade(const PrefixParams& pp, const DecodeParams& dp, int group, bool trace,
                           hipStream_t stream) {
   const int64_t rows = (int64_t)pp.batch * group;
   const int64_t row_groups = (rows + mfma::kPrefixRowsPerWg - 1) / mfma::kPrefixRowsPerWg;
@@ -93,12 +93,14 @@ hipError_t launch_cascade(const PrefixParams& pp, const DecodeParams& dp, int gr
   const int64_t grid = (prefix_runs + group_runs + decode_runs) * dp.num_kv_heads;
   if (grid == 0) return hipSuccess;
   if (grid > 0x7fffffffLL) return hipErrorInvalidValue;
+  auto go = [&](auto kernel) {
+    hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(64 * mfma::kWaves), 0, stream, pp, dp,
+                       (int)prefix_runs, (int)group_runs, (int)decode_runs);
+  };
   if (group == 4)
-    hipLaunchKernelGGL(cascade_kernel<4>, dim3((unsigned)grid), dim3(64 * mfma::kWaves), 0, stream,
-                       pp, dp, (int)prefix_runs, (int)group_runs, (int)decode_runs);
+    trace ? go(cascade_kernel<4, true>) : go(cascade_kernel<4, false>);
   else if (group == 8)
-    hipLaunchKernelGGL(cascade_kernel<8>, dim3((unsigned)grid), dim3(64 * mfma::kWaves), 0, stream,
-                       pp, dp, (int)prefix_runs, (int)group_runs, (int)decode_runs);
+    trace ? go(cascade_kernel<8, true>) : go(cascade_kernel<8, false>);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

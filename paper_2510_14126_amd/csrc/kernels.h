@@ -7,6 +7,9 @@
 
 namespace pa {
 
+// Sets the C ABI's thread-local error message (pa_last_error) and returns code.
+int fail(int code, const char* fmt, ...);
+
 struct DecodeParams {
   const uint16_t* k_pool;        // bf16 [num_blocks][num_kv_heads][16][D]
   const uint16_t* v_pool;        // same layout
@@ -97,7 +100,19 @@ struct PrefixParams {
   int32_t max_group_size;        // max_group_size * G <= 64 (one workgroup per group)
   int32_t group_len;             // a multiple of 16, at most 1024
   float scale_log2;
+  // Index trace (trace launches only): the tiles of prefix partition part,
+  // row group rg, KV head g at trace_prefix + ((part * row_groups + rg) *
+  // num_kv_heads + g) * prefix_trace_tiles triples; those of group k at
+  // trace_group + (k * num_kv_heads + g) * group_trace_tiles triples.
+  int32_t* trace_prefix;
+  int32_t* trace_group;
+  int32_t prefix_trace_tiles;    // part_tokens / 16
+  int32_t group_trace_tiles;     // group_len / 16
 };
+
+// Query rows (sequence x head of one KV head) per workgroup of the shared
+// passes: four wavefronts, one 16-row tile each.
+constexpr int kSharedRowsPerWg = 64;
 
 struct ReduceParams {
   const float* part_o;
@@ -119,7 +134,7 @@ hipError_t launch_decode_valu(const DecodeParams& p, int head_dim, int group, bo
 hipError_t launch_decode_mfma(const DecodeParams& p, bool trace, hipStream_t stream);
 // Shared-prefix pass and per-sequence decode in one launch (head_dim 128;
 // the decode half uses VALU for group 4 and MFMA for group 8).
-hipError_t launch_cascade(const PrefixParams& pp, const DecodeParams& dp, int group,
+hipError_t launch_cascade(const PrefixParams& pp, const DecodeParams& dp, int group, bool trace,
                           hipStream_t stream);
 // Log-sum-exp merge of split-KV partials into the bf16 output.
 hipError_t launch_reduce(const ReduceParams& p, int head_dim, hipStream_t stream);

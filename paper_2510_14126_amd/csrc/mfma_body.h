@@ -603,6 +603,7 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
 // afterwards.  Every row writes its (o, lse) partial for the partition,
 // lse = -inf when it attended to nothing.
 constexpr int kPrefixRowsPerWg = 16 * kWaves;
+static_assert(kPrefixRowsPerWg == kSharedRowsPerWg, "the host sizes traces from kSharedRowsPerWg");
 constexpr int kPrefixLdsBytes = 2 * kPrefixStageBlocks * kPrefixStageBytes;   // two stages
 
 // Rows and tokens of one shared-span workgroup: rows R = row0 .. (16 per
@@ -618,9 +619,9 @@ struct SharedSpan {
   int rot;
 };
 
-template <int G>
+template <int G, bool TRACE>
 __device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, const SharedSpan& sp,
-                                                 lds_u8_t* smem) {
+                                                 lds_u8_t* smem, int32_t* trace) {
   const int lane = threadIdx.x & 63;
   const int wave = wave_uniform(threadIdx.x >> 6);
   const int q = lane >> 4;
@@ -723,6 +724,17 @@ __device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, c
           valid[s] = has ? min(16, end - tb) : 0;
           lim[0][s] = min(valid[s], max(ctx - tb, 0));
           fast = fast && valid[s] == 16 && min_ctx - tb >= 16;
+          if constexpr (TRACE) {
+            // slot = the block's position in the span (not in the walk)
+            const int bi = has ? block_of(i) : 0;
+            const int id = __builtin_amdgcn_readlane(raw, bi);
+            if (has && wave == 0 && lane == 0) {
+              int32_t* tr = trace + 3 * bi;
+              tr[0] = (start >> 4) + bi;
+              tr[1] = id;
+              tr[2] = valid[s];
+            }
+          }
         }
         if (fast)
           tile_core_nb<false, NB>(S, st, vtr, qb, valid, lim, q, n, p.scale_log2);
@@ -757,7 +769,7 @@ __device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, c
 
 // The batch-wide prefix: partition `part` of the prefix against row group
 // `grp` (64 rows) of all B*G query rows of KV head g.
-template <int G>
+template <int G, bool TRACE>
 __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_index, lds_u8_t* smem) {
   const int total_rows = p.batch * G;
   const int groups = (total_rows + kPrefixRowsPerWg - 1) / kPrefixRowsPerWg;
@@ -779,13 +791,16 @@ __device__ __forceinline__ void prefix_mfma_body(const PrefixParams& p, int wg_i
   // all queueing on the L2 lines of the same one.
   const int nblk = (sp.end - sp.start + 15) >> 4;
   sp.rot = (int)(((int64_t)grp * nblk) / groups) % nblk;
-  shared_span_body<G>(p, g, sp, smem);
+  int32_t* tr = nullptr;
+  if constexpr (TRACE)
+    tr = p.trace_prefix + (((size_t)part * groups + grp) * p.num_kv_heads + g) * p.prefix_trace_tiles * 3;
+  shared_span_body<G, TRACE>(p, g, sp, smem, tr);
 }
 
 // The second level: group k's rows (its sequences x G heads of KV head g,
 // at most 64) against the group_len tokens the group shares after the
 // prefix, one partition written to slot prefix_parts.
-template <int G>
+template <int G, bool TRACE>
 __device__ __forceinline__ void group_mfma_body(const PrefixParams& p, int wg_index, lds_u8_t* smem) {
   const int g = wg_index % p.num_kv_heads;
   const int k = wg_index / p.num_kv_heads;
@@ -805,7 +820,10 @@ __device__ __forceinline__ void group_mfma_body(const PrefixParams& p, int wg_in
   sp.bt = p.block_tables + (size_t)s0 * p.bt_stride + (sp.start >> 4);
   sp.part = p.prefix_parts;
   sp.rot = 0;
-  shared_span_body<G>(p, g, sp, smem);
+  int32_t* tr = nullptr;
+  if constexpr (TRACE)
+    tr = p.trace_group + ((size_t)k * p.num_kv_heads + g) * p.group_trace_tiles * 3;
+  shared_span_body<G, TRACE>(p, g, sp, smem, tr);
 }
 
 // Causal attention of a chunk of new tokens over its sequence's paged

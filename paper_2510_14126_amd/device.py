@@ -25,7 +25,7 @@ class PagedBatch:
     def __init__(self, w, device="cuda:0", partition_size: int | None = None,
                  register_blocks: bool = True, k_pool=None, v_pool=None,
                  prefix_len: int = 0, prefix_partition_size: int = 256, schedule: bool = False,
-                 group_start=None, group_len: int = 0):
+                 group_start=None, group_len: int = 0, check_tables: bool = True):
         self.w = w
         self.device = torch.device(device)
         self.partition_size = w.partition_size if partition_size is None else partition_size
@@ -43,6 +43,11 @@ class PagedBatch:
             self.register_placement()
         self.prefix_len = prefix_len
         self.prefix_partition_size = prefix_partition_size
+        if check_tables and (prefix_len or group_len):
+            # the shared passes read shared entries from one row: verify the
+            # host tables really share them before launching
+            binding.paged_attn_check_tables(self.pool, w.block_tables, w.context_lens, prefix_len,
+                                            group_start if group_len else None, group_len)
         # second level: groups of consecutive sequences sharing group_len tokens after the prefix
         self.group_len = group_len
         self.group_start = None
@@ -89,11 +94,15 @@ class PagedBatch:
     def bt_stride(self) -> int:
         return int(self.w.block_tables.shape[1])
 
-    def decode(self, stream=None, out=None) -> None:
+    def decode(self, stream=None, out=None, pool=None, q=None) -> None:
+        """The step's decode launch; ``pool``/``q`` replace the batch's own
+        (a replica of the same data at other addresses)."""
+        pool = self.pool if pool is None else pool
+        q = self.q if q is None else q
         if self.group_len:
             n = 0 if self.items is None else int(self.items.numel())
             binding.paged_attn_decode_cascade_groups(
-                self.pool, self.q, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,
+                pool, q, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,
                 self.w.scale, self.max_ctx, self.partition_size, self.prefix_len,
                 self.prefix_partition_size, self.group_start, self.num_groups, self.max_group_size,
                 self.group_len, self.items if n else None, n, self.part_o, self.part_lse, stream)
@@ -102,22 +111,22 @@ class PagedBatch:
             n = int(self.items.numel())
             if self.prefix_len:
                 binding.paged_attn_decode_cascade_scheduled(
-                    self.pool, self.q, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,
+                    pool, q, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,
                     self.w.scale, self.max_ctx, self.partition_size, self.prefix_len,
                     self.prefix_partition_size, self.items, n, self.part_o, self.part_lse, stream)
             else:
                 binding.paged_attn_decode_scheduled(
-                    self.pool, self.q, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,
+                    pool, q, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,
                     self.w.scale, self.max_ctx, self.partition_size, self.items, n,
                     self.out if out is None else out, self.part_o, self.part_lse, stream)
             return
         if self.prefix_len:
             binding.paged_attn_decode_cascade(
-                self.pool, self.q, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,
+                pool, q, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,
                 self.w.scale, self.max_ctx, self.partition_size, self.prefix_len,
                 self.prefix_partition_size, self.part_o, self.part_lse, stream)
             return
-        binding.paged_attn_decode(self.pool, self.q, self.bt, self.bt_stride, self.ctx, self.batch,
+        binding.paged_attn_decode(pool, q, self.bt, self.bt_stride, self.ctx, self.batch,
                                   self.hq, self.w.scale, self.max_ctx, self.partition_size,
                                   self.out if out is None else out, self.part_o, self.part_lse,
                                   stream)

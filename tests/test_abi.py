@@ -27,7 +27,7 @@ def declared_functions():
 
 def test_header_and_library_agree():
     names = declared_functions()
-    assert len(names) == 29, names
+    assert len(names) == 33, names
     lib = pa.library()
     for n in names:
         assert hasattr(lib, n), f"library does not export {n}"
@@ -412,3 +412,120 @@ def test_grouped_cascade_empty_batch_is_a_no_op():
     p = make_pool()
     pa.paged_attn_decode_cascade_groups(p, 0, 0, 8, 0, 0, 32, 0.1, 128, 64, 64, 64, None, 0, 0, 32,
                                         None, 0, None, None)
+
+
+# ------------------------------------------------------------ table check
+
+def _shared_tables():
+    """Three sequences sharing a 2-block prefix; sequences 1 and 2 form a
+    group sharing one block after it."""
+    bt = np.array([[0, 1, 2, 3, -1],
+                   [0, 1, 4, 5, 6],
+                   [0, 1, 4, 7, -1]], dtype=np.int32)
+    ctx = np.array([64, 80, 60], dtype=np.int32)
+    return bt, ctx
+
+
+def test_check_tables_accepts_shared_prefix_and_groups():
+    p = make_pool(nb=10)
+    bt, ctx = _shared_tables()
+    pa.paged_attn_check_tables(p, bt, ctx)
+    pa.paged_attn_check_tables(p, bt, ctx, prefix_len=32)
+    pa.paged_attn_check_tables(p, bt, ctx, prefix_len=32, group_start=[0, 1, 3], group_len=16)
+
+
+def test_check_tables_rejects_a_prefix_mismatch():
+    p = make_pool(nb=10)
+    bt, ctx = _shared_tables()
+    bt[2, 1] = 8                         # sequence 2's second prefix block differs from row 0
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.paged_attn_check_tables(p, bt, ctx, prefix_len=32)
+    assert e.value.code == pa.PA_EINVAL and e.value.bad_seq == 2
+    assert "block_tables[2][1] = 8" in pa.pa_last_error()
+    pa.paged_attn_check_tables(p, bt, ctx, prefix_len=16)     # the first block still matches
+
+
+def test_check_tables_rejects_a_group_mismatch():
+    p = make_pool(nb=10)
+    bt, ctx = _shared_tables()
+    bt[2, 2] = 9                         # differs from the group's first row (sequence 1)
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.paged_attn_check_tables(p, bt, ctx, prefix_len=32, group_start=[0, 1, 3], group_len=16)
+    assert e.value.bad_seq == 2
+    # as groups of one, nothing is shared after the prefix
+    pa.paged_attn_check_tables(p, bt, ctx, prefix_len=32, group_start=[0, 1, 2, 3], group_len=16)
+
+
+def test_check_tables_short_sequences_only_need_what_they_read():
+    p = make_pool(nb=10)
+    bt, ctx = _shared_tables()
+    ctx[1] = 10                          # inside the first prefix block
+    bt[1, 1] = 9                         # an entry this sequence never reads
+    pa.paged_attn_check_tables(p, bt, ctx, prefix_len=32)
+    ctx[1] = 17                          # now it reads the second block as well
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.paged_attn_check_tables(p, bt, ctx, prefix_len=32)
+    assert e.value.bad_seq == 1
+
+
+@pytest.mark.parametrize("mutate", ["id_out_of_pool", "negative_id", "ctx_past_table", "bad_groups"])
+def test_check_tables_rejects_bad_tables(mutate):
+    p = make_pool(nb=10)
+    bt, ctx = _shared_tables()
+    kw = {}
+    if mutate == "id_out_of_pool":
+        bt[1, 4] = 10
+    elif mutate == "negative_id":
+        bt[2, 3] = -1
+    elif mutate == "ctx_past_table":
+        ctx[0] = 81
+    else:
+        kw = dict(prefix_len=32, group_start=[0, 2, 1, 3], group_len=16)
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.paged_attn_check_tables(p, bt, ctx, **kw)
+    assert e.value.code == pa.PA_EINVAL
+
+
+def test_check_tables_accepts_the_stage_workloads():
+    from workloads import build_config, group_starts
+    for k in (2, 3, 5):
+        w = build_config(k, values=False)
+        p = pa.kv_pool_create(w.num_blocks, 16, w.num_kv_heads, w.head_dim, FAKE_K, FAKE_V)
+        kw = dict(prefix_len=16 * w.meta["prefix_blocks"])
+        if "groups" in w.meta:
+            kw.update(group_start=group_starts(w), group_len=16 * w.meta["mid_blocks"])
+        pa.paged_attn_check_tables(p, w.block_tables, w.context_lens, **kw)
+        p.close()
+
+
+# ------------------------------------------------------------ trace layouts
+
+def test_cascade_trace_layout():
+    p = make_pool(nb=10, hkv=8)
+    lay = pa.paged_attn_cascade_trace_layout(p, 10, 32, 2300, 512, 2048, 512)
+    # prefix: 4 partitions x ceil(40 / 64) = 1 row group x 8 heads x 32 tiles
+    assert lay["prefix_tiles"] == 32 and lay["group_offset"] == 3 * 4 * 1 * 8 * 32
+    assert lay["group_tiles"] == 0 and lay["decode_offset"] == lay["group_offset"]
+    # one 512-token partition after the prefix, 10 sequences, 8 heads, 32 tiles
+    assert lay["decode_tiles"] == 32 and lay["total"] == lay["decode_offset"] + 3 * 10 * 8 * 32
+    g = pa.paged_attn_cascade_trace_layout(p, 40, 64, 3000, 512, 2048, 1024, num_groups=5,
+                                           group_len=256)
+    # 40 x 8 = 320 rows -> 5 row groups; 2 prefix partitions of 64 tiles
+    assert g["group_offset"] == 3 * 2 * 5 * 8 * 64 and g["group_tiles"] == 16
+    assert g["decode_offset"] == g["group_offset"] + 3 * 5 * 8 * 16
+    assert g["total"] == g["decode_offset"] + 3 * 2 * 40 * 8 * 32     # 696 tokens after: 2 parts
+    with pytest.raises(pa.PagedAttnError):
+        pa.paged_attn_cascade_trace_layout(p, 10, 30, 2300, 512, 2048, 512)
+
+
+def test_cascade_trace_capacity_checked():
+    p = make_pool(nb=10, hkv=8)
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.paged_attn_decode_cascade_trace(p, 0x30000, 0x50000, 160, 0x60000, 10, 32, 0.1, 2300, 512,
+                                           2048, 512, None, 0, 0, 0, None, 0, 0xA0000, 0xB0000,
+                                           0xC0000, 100)
+    assert e.value.code == pa.PA_EINVAL and "trace_capacity" in pa.pa_last_error()
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.paged_attn_decode_scheduled_trace(p, 0x1000, 0x2000, 4, 0x3000, 2, 32, 0.1, 64, 0,
+                                             0x4000, 2, 0x4000, None, None, 0x5000, 10)
+    assert e.value.code == pa.PA_EINVAL and "trace_capacity" in pa.pa_last_error()

@@ -23,3 +23,20 @@ def test_private_copies_count_every_sequence():
     per_seq = int(((w.context_lens + 15) // 16).sum())
     assert private == per_seq
     assert shared == per_seq - (w.batch - 1) * (32 // 16)
+
+
+def test_bench_launch_configurations():
+    """The launch bench.py times: stated 512-token partitions on the
+    long-context pool, the cascade wherever a prefix is shared, request groups
+    on the fixer batch."""
+    expect = {1: (512, None, False), 2: (512, 2048, False), 3: (1024, 2048, True),
+              4: (8192, None, False), 5: (512, 4096, False)}
+    for k, (S, L, groups) in expect.items():
+        w = build_config(k, values=False)
+        s, kw = bench.launch_configuration(k, w)
+        assert s == S
+        assert kw.get("prefix_len") == L
+        assert ("group_len" in kw) == groups
+    w = build_config(5, values=False)
+    assert bench.launch_configuration(5, w)[1]["prefix_partition_size"] == 512
+    assert bench.launch_configuration(5, w, cascade="off")[1] == {}

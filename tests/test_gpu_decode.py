@@ -62,33 +62,22 @@ def assert_gate(out_bits, ref, what):
 
 # ------------------------------------------------------------------ configs
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4])
-def test_config_parity_all_outputs(k):
-    say(f"config {k} build")
-    w = build_config(k)
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+def test_config_parity_all_outputs(k, stage_batches):
+    """Every output of each workload through the plain split-KV decode (its
+    stated or default partition size) and the reduce, against the oracle."""
+    w = stage_batches.workload(k)
     say(f"config {k} {w.name}: B={w.batch} Hq={w.num_q_heads} Hkv={w.num_kv_heads} D={w.head_dim} "
         f"NB={w.num_blocks} max_ctx={w.max_context_len} S={w.partition_size}")
     out = gpu_out(w)
-    ref, _ = decode_workload(w)
-    assert_gate(out, ref, f"config {k}")
-
-
-def test_config5_long_context_sampled():
-    say("config 5 build (10.6 GB pool)")
-    w = build_config(5)
-    say(f"config 5: B={w.batch} NB={w.num_blocks} max_ctx={w.max_context_len}")
-    out = gpu_out(w)
-    ctx = w.context_lens
-    rng = np.random.default_rng(5)
-    seqs = sorted({int(np.argmax(ctx)), int(np.argmin(ctx)), *rng.choice(w.batch, 4, replace=False).tolist()})
-    say(f"config 5 oracle on sequences {seqs}")
-    ref, _ = decode_workload(w, seqs=seqs)
-    assert_gate(out[seqs], ref, "config 5 sampled")
-    # every output is a convex combination of V rows: finite and no larger
-    # in magnitude than the largest |V| in the pool (+1 bf16 ulp of rounding)
-    vmax = max(int((w.v_pool[i: i + 8192] & 0x7FFF).max()) for i in range(0, w.num_blocks, 8192))
-    assert np.isfinite(bf16_to_f64(out)).all()
-    assert int((out & 0x7FFF).max()) <= vmax + 1
+    ref, _ = stage_batches.reference(k)
+    assert_gate(out, ref, f"config {k} all {w.batch} sequences")
+    if k == 5:
+        # every output is a convex combination of V rows: finite and no larger
+        # in magnitude than the largest |V| in the pool (+1 bf16 ulp of rounding)
+        vmax = max(int((w.v_pool[i: i + 8192] & 0x7FFF).max()) for i in range(0, w.num_blocks, 8192))
+        assert np.isfinite(bf16_to_f64(out)).all()
+        assert int((out & 0x7FFF).max()) <= vmax + 1
 
 
 # -------------------------------------------------------- shapes and edges
@@ -264,9 +253,9 @@ def test_shared_prefix_equals_duplicated_bit_identical(hq):
 
 
 @pytest.mark.parametrize("k", [2, 1])
-def test_repeat_runs_bit_identical(k):
+def test_repeat_runs_bit_identical(k, stage_batches):
     say(f"determinism config {k}")
-    w = build_config(k)
+    w = stage_batches.workload(k)
     from paper_2510_14126_amd.device import PagedBatch
     pb = PagedBatch(w, DEV)
     outs = []
@@ -401,22 +390,16 @@ def test_growing_scores_force_rescales(S, hq):
 
 # ------------------------------------------------- shared-prefix cascade
 
-@pytest.mark.parametrize("k", [2, 3])
-def test_cascade_stage_configs_all_outputs(k):
-    w = build_config(k)
+@pytest.mark.parametrize("k", [2, 3, 5])
+def test_cascade_stage_configs_all_outputs(k, stage_batches):
+    """The full-grid cascade (no work list) on every workload with a shared
+    prefix, every output against the oracle."""
+    w = stage_batches.workload(k)
     L = w.meta["prefix_blocks"] * 16
-    say(f"cascade config {k} {w.name}: prefix {L}")
-    out = gpu_out(w, prefix_len=L, prefix_partition_size=256)
-    assert_gate(out, decode_workload(w)[0], f"cascade config {k}")
-
-
-def test_cascade_long_context_sampled():
-    say("cascade config 5 build")
-    w = build_config(5)
-    L = w.meta["prefix_blocks"] * 16
-    out = gpu_out(w, prefix_len=L, prefix_partition_size=512)
-    seqs = [0, int(np.argmax(w.context_lens)), int(np.argmin(w.context_lens)), 77]
-    assert_gate(out[seqs], decode_workload(w, seqs=seqs)[0], "cascade config 5 sampled")
+    pps = 512 if k == 5 else 256
+    say(f"cascade config {k} {w.name}: prefix {L}, prefix partitions {pps}")
+    out = gpu_out(w, prefix_len=L, prefix_partition_size=pps)
+    assert_gate(out, stage_batches.reference(k)[0], f"cascade config {k} all {w.batch} sequences")
 
 
 CASCADE_CASES = [

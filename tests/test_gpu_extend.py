@@ -133,3 +133,41 @@ def test_extend_scale_sign(factor):
     w, q, q_start = make_extend(71, ctx, chunk, poison=True)
     w.scale = float(w.scale) * factor
     check(w, q, q_start, f"scale x{factor}")
+
+
+LONG = [
+    # contexts in (4096, 8192] (exactly 8192 included), chunks of at least 1024
+    # tokens: the block-id staging takes a second pass above 4096 tokens
+    ("long contexts", [8192, 6000, 4097, 7777], [1024, 2000, 1100, 1500]),
+    ("one full-length chunk", [8192], [8192]),
+]
+
+
+@pytest.mark.parametrize("hq", [32, 64], ids=["g4", "g8"])
+@pytest.mark.parametrize("name,ctx,chunk", LONG, ids=[c[0] for c in LONG])
+def test_extend_long_contexts(name, ctx, chunk, hq, oracle_pool):
+    say(f"extend {name} hq={hq}: ctx={ctx} chunk={chunk}")
+    w, q, q_start = make_extend(91, ctx, chunk, hq=hq, prefix_len=2048, poison=True)
+    out = gpu_extend(w, q, q_start)
+    ref, _ = oracle_pool.extend(q, q_start, w.k_pool, w.v_pool, w.block_tables, w.context_lens,
+                                w.scale)
+    rep = compare(out, ref)
+    say(f"{name} g{hq // 8}: {rep}")
+    assert rep.passed, f"{name}: {rep}"
+
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_extend_bench_batches_all_rows(k, stage_batches, oracle_pool):
+    """The batches bench.py --extend times (each sequence's tokens after its
+    shared prompt as the chunk, its seeded queries), every output row."""
+    import bench
+    w = stage_batches.workload(k)
+    chunk, q_start, q = bench.extend_inputs(w)
+    say(f"extend bench batch config {k}: {int(q_start[-1])} rows, chunks "
+        f"{int(chunk.min())}..{int(chunk.max())}")
+    out = gpu_extend(w, q, q_start)
+    ref, _ = oracle_pool.extend(q, q_start, w.k_pool, w.v_pool, w.block_tables, w.context_lens,
+                                w.scale)
+    rep = compare(out, ref)
+    say(f"extend bench batch config {k}, all rows: {rep}")
+    assert rep.passed, f"config {k}: {rep}"

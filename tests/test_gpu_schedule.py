@@ -18,7 +18,7 @@ sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 
 import bench  # noqa: E402
 from oracle import compare, decode_workload  # noqa: E402
-from workloads import build_config, group_starts, logical_case, page_case  # noqa: E402
+from workloads import logical_case, page_case  # noqa: E402
 
 DEV = "cuda:0"
 
@@ -36,23 +36,16 @@ def _gpu():
 
 
 @pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
-def test_bench_launch_configurations(k):
+def test_bench_launch_configurations(k, stage_batches):
     """Each workload in the launch configuration bench.py times (partition
-    sizes, shared-prefix cascade, work list), against the oracle: every
-    output of the small workloads, sampled sequences of the large ones."""
-    w = build_config(k)
-    S = bench.DEFAULT_PARTITION[k]
-    L = 16 * int(w.meta.get("prefix_blocks", 0))
-    kw = dict(prefix_len=L, prefix_partition_size=bench.default_prefix_partition(k, L)) if L else {}
-    if L and "groups" in w.meta and w.meta.get("mid_blocks", 0):     # as bench.py --groups auto
-        kw.update(group_start=group_starts(w), group_len=16 * int(w.meta["mid_blocks"]))
+    sizes, shared-prefix cascade with request groups, work list): every
+    output against the oracle."""
+    w = stage_batches.workload(k)
+    S, kw = bench.launch_configuration(k, w)
     say(f"bench launch configuration {k} {w.name}: S={S} {sorted(kw)}")
     out = outputs(w, S, items=True, **kw)
-    ctx = w.context_lens
-    seqs = None if k <= 3 else sorted({0, int(np.argmax(ctx)), int(np.argmin(ctx)), w.batch // 2,
-                                       w.batch - 1})
-    rep = compare(out if seqs is None else out[seqs], decode_workload(w, seqs=seqs)[0])
-    say(f"bench configuration {k} vs oracle: {rep}")
+    rep = compare(out, stage_batches.reference(k)[0])
+    say(f"bench configuration {k} vs oracle, all {w.batch} sequences: {rep}")
     assert rep.passed
 
 
@@ -76,39 +69,37 @@ def assert_same(a, b, what):
 
 
 @pytest.mark.parametrize("k", [1, 2, 3, 4])
-def test_scheduled_configs_bit_identical(k):
-    w = build_config(k)
+def test_scheduled_configs_bit_identical(k, stage_batches):
+    w = stage_batches.workload(k)
     say(f"scheduled config {k} {w.name}")
     plain = outputs(w)
     sched = outputs(w, items=True)
     assert_same(sched, plain, f"config {k}")
-    if k <= 2:
-        rep = compare(sched, decode_workload(w)[0])
-        say(f"config {k} vs oracle: {rep}")
-        assert rep.passed
+    rep = compare(sched, stage_batches.reference(k)[0])
+    say(f"config {k} vs oracle: {rep}")
+    assert rep.passed
 
 
 @pytest.mark.parametrize("k", [2, 3])
-def test_scheduled_cascade_configs_bit_identical(k):
-    w = build_config(k)
+def test_scheduled_cascade_configs_bit_identical(k, stage_batches):
+    w = stage_batches.workload(k)
     L = w.meta["prefix_blocks"] * 16
     say(f"scheduled cascade config {k}: prefix {L}")
     kw = dict(prefix_len=L, prefix_partition_size=256)
     assert_same(outputs(w, items=True, **kw), outputs(w, **kw), f"cascade config {k}")
 
 
-def test_scheduled_long_context_bit_identical():
-    say("scheduled config 5 build")
-    w = build_config(5)
+def test_scheduled_long_context_bit_identical(stage_batches):
+    w = stage_batches.workload(5)
+    say("scheduled config 5")
     L = w.meta["prefix_blocks"] * 16
     plain = outputs(w, 512)
     assert_same(outputs(w, 512, items=True), plain, "config 5")
     kw = dict(prefix_len=L, prefix_partition_size=512)
     casc = outputs(w, 512, items=True, **kw)
     assert_same(casc, outputs(w, 512, **kw), "cascade config 5")
-    seqs = [0, int(np.argmax(w.context_lens)), int(np.argmin(w.context_lens)), 77]
-    rep = compare(casc[seqs], decode_workload(w, seqs=seqs)[0])
-    say(f"cascade config 5 sampled vs oracle: {rep}")
+    rep = compare(casc, stage_batches.reference(5)[0])
+    say(f"scheduled cascade config 5 vs oracle, all sequences: {rep}")
     assert rep.passed
 
 
