@@ -28,9 +28,10 @@
 // The online softmax keeps one running max per query row, replicated over the
 // four lane groups, and rescales the accumulator only when a block raises the
 // max by more than kLazyRescale (log2 units): probabilities stay <= 2^8, the
-// rescale branch is wave-uniform and rare.  P is rounded to bf16 for the
-// matrix core and the row sum adds the same rounded values, so the result is
-// an exact convex combination of the V rows up to fp32 accumulation.
+// rescale branch is wave-uniform and rare.  Each probability reaches the
+// matrix core as a bf16 pair (high part and the rounded remainder, two MFMAs
+// per PV step), which carries it to about 2^-17 relative; the row sum adds the
+// fp32 values.
 // Tail rows are removed by select: score -inf and V row zero.
 #pragma once
 
@@ -162,18 +163,24 @@ __device__ __forceinline__ void tile_core(MfmaState<NT>& S, const u32x4_t (&ka)[
     }
   }
 
-  // Probabilities, rounded to bf16 for the matrix core; the column sum uses
-  // the same rounded values, summed from the packed words by v_dot2 against
-  // (1, 1).
-  short4_t pa[NT];
+  // Probabilities as bf16 pairs for the matrix core: p = hi + lo, hi = bf16(p)
+  // and lo = bf16(p - hi) (the difference is exact in fp32), so the PV
+  // product sees each weight to about 2^-17 relative; the column sum adds the
+  // fp32 values.
+  short4_t pa[NT], pl[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     const float mref = S.m[t] == -__builtin_inff() ? 0.f : S.m[t];  // fully masked: p = 0
+    float ps = 0.f;
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      pa[t][r] = __builtin_bit_cast(short, (__bf16)fast_exp2(sc[t][r] - mref));
-    const uint2 pw = __builtin_bit_cast(uint2, pa[t]);
-    S.l[t] = dot2_bf16(pw.y, 0x3F803F80u, dot2_bf16(pw.x, 0x3F803F80u, S.l[t]));
+    for (int r = 0; r < 4; ++r) {
+      const float pf = fast_exp2(sc[t][r] - mref);
+      const __bf16 hi = (__bf16)pf;
+      pa[t][r] = __builtin_bit_cast(short, hi);
+      pl[t][r] = __builtin_bit_cast(short, (__bf16)(pf - (float)hi));
+      ps += pf;
+    }
+    S.l[t] += ps;
   }
 
   // PV: instruction j takes B = V[token 4e+q][dim 8n+j], e = 0..3: bf16 j of
@@ -194,8 +201,10 @@ __device__ __forceinline__ void tile_core(MfmaState<NT>& S, const u32x4_t (&ka)[
     const uint32_t hi = __builtin_amdgcn_perm(vw[3][j >> 1], vw[2][j >> 1], sel);
     const short4_t vb = __builtin_bit_cast(short4_t, make_uint2(lo, hi));
 #pragma unroll
-    for (int t = 0; t < NT; ++t)
+    for (int t = 0; t < NT; ++t) {
       S.o[t][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa[t], vb, S.o[t][j], 0, 0, 0);
+      S.o[t][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pl[t], vb, S.o[t][j], 0, 0, 0);
+    }
   }
 }
 
@@ -308,10 +317,11 @@ __device__ __forceinline__ void tile_core_nb(MfmaState<NT>& S, const lds_u8_t* s
         a[t][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[b][c]),
                                                           __builtin_bit_cast(bf16x8_t, qb[t][c]), a[t][b], 0, 0, 0);
 
-  // Probabilities of tile t rounded to bf16 (the A operands: element e of
-  // pa[t][p] is the score 8p + e); the column sum uses the same rounded
-  // values, from the packed words by v_dot2 against (1, 1).
-  bf16x8_t pa[NT][NB / 2];
+  // Probabilities of tile t as bf16 pairs (the A operands: element e of
+  // pa[t][p] and pl[t][p] is the high and low part of the weight of score
+  // 8p + e, p = hi + lo to about 2^-17 relative); the column sum adds the fp32
+  // values.
+  bf16x8_t pa[NT][NB / 2], pl[NT][NB / 2];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     float sc[4 * NB];   // scaled scores, or raw ones with FOLD
@@ -370,11 +380,12 @@ __device__ __forceinline__ void tile_core_nb(MfmaState<NT>& S, const lds_u8_t* s
         } else {
           ex = sc[8 * pp + e] - mref;
         }
-        pa[t][pp][e] = (__bf16)fast_exp2(ex);
+        const float pf = fast_exp2(ex);
+        const __bf16 hi = (__bf16)pf;
+        pa[t][pp][e] = hi;
+        pl[t][pp][e] = (__bf16)(pf - (float)hi);
+        lsum += pf;
       }
-      const u32x4_t pw = __builtin_bit_cast(u32x4_t, pa[t][pp]);
-#pragma unroll
-      for (int w = 0; w < 4; ++w) lsum = dot2_bf16(pw[w], 0x3F803F80u, lsum);
     }
     S.l[t] += lsum;
   }
@@ -405,9 +416,12 @@ __device__ __forceinline__ void tile_core_nb(MfmaState<NT>& S, const lds_u8_t* s
       const u32x4_t vb = {b0.x & mlo[2 * pp], b0.y & mhi[2 * pp], b1.x & mlo[2 * pp + 1],
                           b1.y & mhi[2 * pp + 1]};
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
+      for (int t = 0; t < NT; ++t) {
         S.o[t][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[t][pp], __builtin_bit_cast(bf16x8_t, vb),
                                                             S.o[t][j], 0, 0, 0);
+        S.o[t][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl[t][pp], __builtin_bit_cast(bf16x8_t, vb),
+                                                            S.o[t][j], 0, 0, 0);
+      }
     }
   }
 }

@@ -23,10 +23,12 @@
 //    query rows and its K row quads in a lane-dependent order (row r ^ c/4,
 //    quad u ^ tg(c)), so every level keeps the same slots on both partners.
 //  * PV: lane (J, c) accumulates its dims over tokens = J mod 4, two tokens
-//    per v_dot2c_f32_bf16: probabilities are rounded to bf16 (the row sum adds
-//    the same rounded values, so the weights stay an exact convex combination)
-//    and packed in pairs (tokens 4(2h)+J, 4(2h+1)+J) by the even lane of each
-//    lane pair; one v_perm_b32 pairs the V values of those tokens for one dim.
+//    per v_dot2c_f32_bf16: each probability is split into a bf16 high part
+//    and the bf16-rounded remainder (about 2^-17 relative together; the row
+//    sum adds the fp32 values), the parts are packed in pairs (tokens
+//    4(2h)+J, 4(2h+1)+J) by the even lane of each lane pair and each pair
+//    takes one dot2; one v_perm_b32 pairs the V values of those tokens for
+//    one dim.
 //    The packed probabilities of row r sit in the same row group at a fixed
 //    position, so one DPP row broadcast delivers them.  The four row groups
 //    are summed once, at the end.
@@ -168,18 +170,24 @@ __device__ __forceinline__ void process_tile(WaveState<D, G>& S, const KvTile<D>
     });
   }
 
-  // Probabilities rounded to bf16; even lanes then hold the packed pair
-  // (even token quad, odd token quad) of their row: the lane's own quad is
-  // even unless bit 2 of c is set.
+  // Probabilities as bf16 pairs: p = hi + lo with hi = bf16(p) and lo =
+  // bf16(p - hi) (the difference is exact in fp32), about 2^-17 relative; the
+  // row sum adds the fp32 values.  Even lanes then hold the packed high parts
+  // (even token quad, odd token quad) of their row, and likewise the low
+  // parts: the lane's own quad is even unless bit 2 of c is set.
   const uint32_t pack_sel = ((c >> 2) & 1) ? 0x03020706u : 0x07060302u;
-  float pk[R];
+  float pk[R], pkl[R];
 #pragma unroll
   for (int k = 0; k < R; ++k) {
     const float mref = S.m[k] == -__builtin_inff() ? 0.f : S.m[k];
-    const uint32_t pb = bf16_rne(fast_exp2(sc[k] - mref)) << 16;
-    S.l[k] += __uint_as_float(pb);
+    const float pf = fast_exp2(sc[k] - mref);
+    const uint32_t pb = bf16_rne(pf) << 16;
+    const uint32_t lb = bf16_rne(pf - __uint_as_float(pb)) << 16;
+    S.l[k] += pf;
     const uint32_t nb = __float_as_uint(dpp<kDppQuadXor1>(__uint_as_float(pb)));
+    const uint32_t nl = __float_as_uint(dpp<kDppQuadXor1>(__uint_as_float(lb)));
     pk[k] = __uint_as_float(__builtin_amdgcn_perm(nb, pb, pack_sel));
+    pkl[k] = __uint_as_float(__builtin_amdgcn_perm(nl, lb, pack_sel));
   }
 
   // PV: step h covers tokens 4(2h)+J and 4(2h+1)+J; row r's packed pair is at
@@ -198,8 +206,9 @@ __device__ __forceinline__ void process_tile(WaveState<D, G>& S, const KvTile<D>
     static_for<0, G>([&](auto rc) {
       constexpr int r = decltype(rc)::value;
       const uint32_t pp = __float_as_uint(row_bcast<pair_pos<r % 4, h>()>(pk[r / 4]));
+      const uint32_t pl = __float_as_uint(row_bcast<pair_pos<r % 4, h>()>(pkl[r / 4]));
 #pragma unroll
-      for (int d = 0; d < DPL; ++d) S.acc[r][d] = dot2_bf16(pp, vp[d], S.acc[r][d]);
+      for (int d = 0; d < DPL; ++d) S.acc[r][d] = dot2_bf16(pl, vp[d], dot2_bf16(pp, vp[d], S.acc[r][d]));
     });
   });
 }
