@@ -449,6 +449,33 @@ int paged_attn_check_tables(const pa_kv_pool *pool, const int32_t *block_tables,
                             int32_t *bad_seq_out);
 
 /* ---------------------------------------------------------------------------
+ * A decode step that allocates nothing.
+ *
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.
+ * ------------------------------------------------------------------------- */
+
+/* Bytes of the library's own scratch array per GPU (held from the first call
+ * on a GPU until the process ends). */
+#define PA_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* paged_attn_decode followed, when the batch splits, by paged_attn_reduce,
+ * with the split-KV partials in the library's scratch array instead of
+ * caller buffers: writes out (bf16 [batch][num_q_heads][head_dim]) for every
+ * batch, split or not.  Arguments as in paged_attn_decode.  Calls no
+ * hipMalloc, hipFree or allocating routine; the array's device address is
+ * looked up on the first call on each GPU (the current device).  Returns
+ * PA_EINVAL, before any HIP call, when the partials (paged_attn_workspace_size,
+ * the lse part 256-byte aligned after the outputs) exceed
+ * PA_NOALLOC_SCRATCH_BYTES.  Every call on a GPU uses the same array: calls
+ * that overlap on one GPU (other streams, other threads) race; calls in order
+ * on one stream do not. */
+int paged_attn_decode_noalloc(const pa_kv_pool *pool, const void *q, const int32_t *block_tables,
+                              int32_t bt_stride, const int32_t *context_lens, int32_t batch,
+                              int32_t num_q_heads, float scale, int32_t max_context_len,
+                              int32_t partition_size, void *out, void *stream);
+
+/* ---------------------------------------------------------------------------
  * KV append.
  *
  * Every decode step adds the key and value rows of the token it produced to

@@ -70,6 +70,8 @@ SIGNATURES = {
     "paged_attn_decode_cascade_trace": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32,
                                                  _i32, _i32, _i32, _vp, _i32, _i32, _i32, _vp, _i32,
                                                  _vp, _vp, _vp, _i64, _vp]),
+    "paged_attn_decode_noalloc": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32, _i32,
+                                           _vp, _vp]),
     "paged_attn_check_tables": (_c_int, [_vp, _pi32, _i32, _pi32, _i32, _i32, _pi32, _i32, _i32,
                                          _pi32]),
     "paged_attn_cascade_workspace_size": (_c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _i32,
@@ -437,3 +439,14 @@ def paged_attn_check_tables(pool: KVPool, block_tables, context_lens, prefix_len
         err = PagedAttnError(rc, _lib.pa_last_error().decode())
         err.bad_seq = bad.value
         raise err
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def paged_attn_decode_noalloc(pool: KVPool, q, block_tables, bt_stride, context_lens, batch,
+                              num_q_heads, scale, max_context_len, partition_size, out,
+                              stream=None) -> None:
+    _check(_lib.paged_attn_decode_noalloc(pool._handle(), _ptr(q), _ptr(block_tables), bt_stride,
+                                          _ptr(context_lens), batch, num_q_heads, scale,
+                                          max_context_len, partition_size, _ptr(out), _ptr(stream)))

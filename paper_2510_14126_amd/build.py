@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB_PATH = os.path.join(HERE, "libpaged_attn.so")
 SOURCES = ["api.cpp", "decode_valu.hip", "decode_mfma.hip", "cascade.hip", "reduce.hip", "append.hip", "extend.hip",
-           "stream_copy.hip", "gather_tiles.hip"]
+           "stream_copy.hip", "gather_tiles.hip", "noalloc.hip"]
 ARCH = "gfx950"
 
 COMMON_FLAGS = [

@@ -27,7 +27,7 @@ def declared_functions():
 
 def test_header_and_library_agree():
     names = declared_functions()
-    assert len(names) == 33, names
+    assert len(names) == 34, names
     lib = pa.library()
     for n in names:
         assert hasattr(lib, n), f"library does not export {n}"
@@ -529,3 +529,16 @@ def test_cascade_trace_capacity_checked():
         pa.paged_attn_decode_scheduled_trace(p, 0x1000, 0x2000, 4, 0x3000, 2, 32, 0.1, 64, 0,
                                              0x4000, 2, 0x4000, None, None, 0x5000, 10)
     assert e.value.code == pa.PA_EINVAL and "trace_capacity" in pa.pa_last_error()
+
+
+def test_noalloc_rejects_partials_beyond_the_scratch_array():
+    """Checked on the host before any HIP call: 64 MiB hold the partials of
+    the stage batches at 512-token partitions up to the fixer's, not more."""
+    p = make_pool(nb=10)
+    with pytest.raises(pa.PagedAttnError) as e:
+        # 256 x 32 heads x 16 partitions x (128 + 1) fp32 > 64 MiB
+        pa.paged_attn_decode_noalloc(p, 0x30000, 0x50000, 512, 0x60000, 256, 32, 0.1, 8192, 512,
+                                     0x70000)
+    assert e.value.code == pa.PA_EINVAL and "scratch" in pa.pa_last_error()
+    ob, lb = pa.paged_attn_workspace_size(160, 32, 128, 3328, 512)
+    assert -(-ob // 256) * 256 + lb <= pa.NOALLOC_SCRATCH_BYTES
