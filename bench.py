@@ -475,68 +475,242 @@ def _blocks_in_use(w) -> int:
     return int(in_use)
 
 
-def _time_steps(w, prefix_len, pps, steps, warmup):
+FOOTPRINT_BUDGETS = (1024, 2048, 4096)   # KV blocks per engine replica and layer (64 KiB each)
+_FP_HQ, _FP_HKV, _FP_D = 32, 8, 128         # head geometry of the generator and fixer stages
+
+
+class Replica:
+    """One engine replica of a stage pool: a host-side block allocator over a
+    fixed KV budget, the prompt contexts it keeps resident, and the sequences
+    it admitted.  Shared prompt blocks are allocated once and retained once
+    per sequence that maps them; with ``private`` every sequence holds its own
+    copy of its prompt blocks (no prefix sharing)."""
+
+    def __init__(self, budget, stages, private=False):
+        from paper_2510_14126_amd import binding
+        from workloads import FIXER_PROMPT, GENERATOR_PROMPT
+        self.b = binding
+        self.budget = budget
+        self.stages = tuple(stages)
+        self.private = private
+        self.pool = binding.kv_pool_create(budget, 16, _FP_HKV, _FP_D, 0x10000, 0x20000)
+        self.prompt = {}
+        if not private:
+            for st, tokens in (("generator", GENERATOR_PROMPT), ("fixer", FIXER_PROMPT)):
+                if st in self.stages:
+                    self.prompt[st] = binding.kv_pool_alloc(self.pool, tokens // 16)
+        self.prompt_blocks = sum(len(v) for v in self.prompt.values())
+        self.seqs = {"generator": [], "fixer": []}    # stage -> [(table ids, context length)]
+        self.groups = []                              # fixer: sequences per request, in order
+
+    def free(self) -> int:
+        return self.b.kv_pool_num_free(self.pool)
+
+    def need(self, unit) -> int:
+        """Blocks a generator call or a whole fixer request (all retries) takes."""
+        from workloads import FIRST_ATTEMPT, FIXER_PROMPT, GENERATOR_PROMPT
+        stage, suffixes = unit
+        nb = lambda t: -(-t // 16)                     # noqa: E731
+        plen = GENERATOR_PROMPT if stage == "generator" else FIXER_PROMPT
+        first = FIRST_ATTEMPT if stage == "fixer" else 0
+        if self.private:
+            return sum(nb(plen) + nb(first) + nb(s) for s in suffixes)
+        return nb(first) + sum(nb(s) for s in suffixes)
+
+    def admit(self, unit) -> bool:
+        """Admit a generator call or a whole fixer request (all retries), or
+        nothing if its blocks do not fit in the free blocks."""
+        from workloads import FIRST_ATTEMPT, FIXER_PROMPT, GENERATOR_PROMPT
+        stage, suffixes = unit
+        if stage not in self.stages or self.need(unit) > self.free():
+            return False
+        nb = lambda t: -(-t // 16)                     # noqa: E731
+        plen = GENERATOR_PROMPT if stage == "generator" else FIXER_PROMPT
+        first = FIRST_ATTEMPT if stage == "fixer" else 0
+        shared_first = [] if self.private or not first else self.b.kv_pool_alloc(self.pool, nb(first))
+        for s in suffixes:
+            if self.private:
+                ids = self.b.kv_pool_alloc(self.pool, nb(plen) + nb(first) + nb(s))
+            else:
+                self.b.kv_pool_retain(self.pool, self.prompt[stage])
+                if shared_first:
+                    self.b.kv_pool_retain(self.pool, shared_first)
+                ids = list(self.prompt[stage]) + list(shared_first) + self.b.kv_pool_alloc(self.pool, nb(s))
+            self.seqs[stage].append((ids, plen + first + s))
+        if stage == "fixer":
+            self.groups.append(len(suffixes))
+        return True
+
+    @property
+    def sequences(self) -> int:
+        return sum(len(v) for v in self.seqs.values())
+
+    def blocks_used(self) -> int:
+        return self.budget - self.free()
+
+    def close(self) -> None:
+        self.pool.close()
+
+
+def footprint_deployments(budget, units):
+    """Three two-replica deployments with the same total KV budget (2 x
+    budget blocks) serving the same demand, a sequence of requests that each
+    make one generator call and one fixer request (units 2i, 2i + 1); each
+    admits whole requests in order until the next no longer fits:
+      isolated  a generator pool and a fixer pool, each keeping its own stage's
+                prompt resident once; the 2 x budget blocks are split between
+                them in proportion to the demand (each stage pool scaled on its
+                own), so both stages admit the same requests;
+      shared    two replicas of one engine, each keeping both stages' prompts
+                resident, taking the requests alternately;
+      private   the shared engine without prefix sharing (every sequence holds
+                its own prompt blocks)."""
+    pairs = [(units[i], units[i + 1]) for i in range(0, len(units) - 1, 2)]
+    # isolated: the most requests whose two stage pools fit in 2 x budget
+    from workloads import FIXER_PROMPT, GENERATOR_PROMPT
+    need_g, need_f = GENERATOR_PROMPT // 16, FIXER_PROMPT // 16
+    k = 0
+    pg, pf = Replica(2 * budget, ["generator"]), Replica(2 * budget, ["fixer"])
+    for gu, fu in pairs:
+        if need_g + pg.need(gu) + need_f + pf.need(fu) > 2 * budget:
+            break
+        need_g += pg.need(gu)
+        need_f += pf.need(fu)
+        k += 1
+    pg.close()
+    pf.close()
+    spare = 2 * budget - need_g - need_f
+    iso = [Replica(need_g + spare // 2, ["generator"]), Replica(need_f + spare - spare // 2, ["fixer"])]
+    for gu, fu in pairs[:k]:
+        assert iso[0].admit(gu) and iso[1].admit(fu)
+    out = {"isolated": iso}
+    for kind, private in (("shared", False), ("private", True)):
+        reps = [Replica(budget, ["generator", "fixer"], private) for _ in range(2)]
+        full = [False, False]
+        for j, (gu, fu) in enumerate(pairs):
+            r = j % 2                          # requests alternate between the replicas
+            if full[r]:
+                r = 1 - r
+            if full[r]:
+                break
+            if reps[r].need(gu) + reps[r].need(fu) > reps[r].free():
+                full[r] = True
+                continue
+            assert reps[r].admit(gu) and reps[r].admit(fu)
+        out[kind] = reps
+    return out
+
+
+def _replica_batches(rep, k_np, v_np, seed):
+    """Decode launches of one replica's step: [(workload, PagedBatch keywords)]."""
+    from workloads import FIRST_ATTEMPT, FIXER_PROMPT, GENERATOR_PROMPT, batch_from_tables
+    out = []
+    if rep.private:
+        seqs = rep.seqs["generator"] + rep.seqs["fixer"]
+        if seqs:
+            w = batch_from_tables("private", [s[0] for s in seqs], [s[1] for s in seqs], rep.budget,
+                                  _FP_HQ, _FP_HKV, _FP_D, seed, k_np, v_np)
+            out.append((w, dict(partition_size=512)))
+        return out
+    gen = rep.seqs["generator"]
+    if gen:
+        w = batch_from_tables("generator", [s[0] for s in gen], [s[1] for s in gen], rep.budget,
+                              _FP_HQ, _FP_HKV, _FP_D, seed, k_np, v_np)
+        out.append((w, dict(partition_size=512, prefix_len=GENERATOR_PROMPT, prefix_partition_size=512)))
+    fix = rep.seqs["fixer"]
+    if fix:
+        w = batch_from_tables("fixer", [s[0] for s in fix], [s[1] for s in fix], rep.budget,
+                              _FP_HQ, _FP_HKV, _FP_D, seed + 1, k_np, v_np)
+        starts = np.concatenate([[0], np.cumsum(rep.groups)]).astype(np.int32)
+        out.append((w, dict(partition_size=1024, prefix_len=FIXER_PROMPT, prefix_partition_size=1024,
+                            group_start=starts, group_len=FIRST_ATTEMPT)))
+    return out
+
+
+def _time_replica(rep, k_np, v_np, steps, warmup, seed):
+    """Microseconds per decode step of one replica's admitted batch (all its
+    launches), rotating over copies of its pool so that no step finds its
+    blocks in the Infinity Cache.  k_np, v_np: the replica's pool values, one
+    block per block of its budget."""
     import torch
     from paper_2510_14126_amd.device import PagedBatch
-    pb = PagedBatch(w, torch.device("cuda:0"), prefix_len=prefix_len, prefix_partition_size=pps)
-    for _ in range(warmup):
-        pb.run()
+    if k_np.shape[0] != rep.budget or v_np.shape[0] != rep.budget:
+        raise ValueError(f"pool values hold {k_np.shape[0]} blocks, the replica {rep.budget}")
+    dev = torch.device("cuda:0")
+    batches = _replica_batches(rep, k_np, v_np, seed)
+    if not batches:
+        return 0.0
+    k0 = torch.from_numpy(k_np.view(np.int16)).to(dev)
+    v0 = torch.from_numpy(v_np.view(np.int16)).to(dev)
+    R = max(1, min(8, -(-(1 << 30) // (2 * k0.numel() * 2))))
+    copies = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(R - 1)]
+    pbs = [[PagedBatch(w, dev, register_blocks=False, k_pool=k, v_pool=v, schedule=True, **kw)
+            for w, kw in batches] for k, v in copies]
+
+    def step(i):
+        for pb in pbs[i % R]:
+            pb.run()
+    for i in range(warmup):
+        step(i)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    for _ in range(steps):
-        pb.run()
+    for i in range(steps):
+        step(i)
     e1.record()
     torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / steps
-    pb.close()
-    return ms
+    us = 1e3 * e0.elapsed_time(e1) / steps
+    for row in pbs:
+        for pb in row:
+            pb.close()
+    del pbs, copies, k0, v0
+    torch.cuda.empty_cache()
+    return us
 
 
 def run_footprint(args):
-    """Analogue of the paper's isolated-vs-shared comparison (Fig. 2) on the
-    synthetic stage batches.  Isolated: each stage pool stores its shared
-    prompt blocks once (referenced from every table) and decodes with the
-    shared-prefix cascade.  Shared engine: every sequence holds private copies
-    of its blocks (the shared-pool reading) and decodes with the plain split-KV
-    kernel.  Block counts come from the pool allocator; throughput is measured."""
-    from workloads import CONFIG_NAMES, build_config, duplicate_shared_blocks
-    per_stage = {}
-    tot = dict(blocks_isolated=0, blocks_private=0, seqs=0, ms_isolated=0.0, ms_private=0.0)
-    for k in (2, 3):
-        w = build_config(k)
-        w.partition_size = DEFAULT_PARTITION.get(k, w.partition_size)
-        wd = duplicate_shared_blocks(w)
-        prefix_len = 16 * int(w.meta.get("prefix_blocks", 0))
-        b_iso, b_priv = _blocks_in_use(w), _blocks_in_use(wd)
-        ms_iso = _time_steps(w, prefix_len, default_prefix_partition(k, prefix_len), args.steps, args.warmup)
-        ms_priv = _time_steps(wd, 0, 256, args.steps, args.warmup)
-        bpb = 2 * w.num_kv_heads * 16 * w.head_dim * 2        # K+V bytes per block and layer
-        per_stage[CONFIG_NAMES[k]] = {
-            "sequences": w.batch, "blocks_isolated": b_iso, "blocks_private": b_priv,
-            "kv_mb_per_layer_isolated": round(b_iso * bpb / 1e6, 1),
-            "kv_mb_per_layer_private": round(b_priv * bpb / 1e6, 1),
-            "us_per_step_isolated": round(ms_iso * 1e3, 2), "us_per_step_private": round(ms_priv * 1e3, 2),
-            "tokens_per_s_isolated": round(w.batch / (ms_iso * 1e-3), 1),
-            "tokens_per_s_private": round(w.batch / (ms_priv * 1e-3), 1)}
-        log(f"footprint {CONFIG_NAMES[k]}: {per_stage[CONFIG_NAMES[k]]}")
-        tot["blocks_isolated"] += b_iso
-        tot["blocks_private"] += b_priv
-        tot["seqs"] += w.batch
-        tot["ms_isolated"] += ms_iso
-        tot["ms_private"] += ms_priv
+    """Analogue of the paper's isolated-vs-shared comparison (Fig. 2, section 2
+    "Cortex Benefits"): under a fixed KV budget per engine replica, how many
+    sequences each deployment admits (the pool allocator's block counts) and
+    the decode tokens/s it sustains at that batch (measured)."""
+    from workloads import normal_bf16, stage_units
+    units = stage_units(2510, 4000)
+    results = []
+    for M in FOOTPRINT_BUDGETS:
+        deps = footprint_deployments(M, units)
+        entry = {"blocks_per_replica": M, "total_blocks": 2 * M,
+                 "mb_per_replica_and_layer": round(M * 2 * _FP_HKV * 16 * _FP_D * 2 / 1e6, 1)}
+        for kind, reps in deps.items():
+            recs = []
+            for i, rep in enumerate(reps):
+                shape = (rep.budget, _FP_HKV, 16, _FP_D)      # the replica's own pool
+                k_np, v_np = normal_bf16(shape, 77, 1), normal_bf16(shape, 77, 2)
+                us = _time_replica(rep, k_np, v_np, args.steps, args.warmup, 300 + i)
+                recs.append({"stages": list(rep.stages), "prompt_blocks": rep.prompt_blocks,
+                             "blocks_used": rep.blocks_used(),
+                             "generator_sequences": len(rep.seqs["generator"]),
+                             "fixer_sequences": len(rep.seqs["fixer"]),
+                             "us_per_step": round(us, 2),
+                             "tokens_per_s": round(rep.sequences / (us * 1e-6), 1) if us else 0.0})
+                rep.close()
+            entry[kind] = {"replicas": recs, "requests": len([1 for r in reps for _ in r.groups]),
+                           "sequences": sum(r["generator_sequences"] + r["fixer_sequences"] for r in recs),
+                           "prompt_blocks": sum(r["prompt_blocks"] for r in recs),
+                           "tokens_per_s": round(sum(r["tokens_per_s"] for r in recs), 1)}
+        entry["isolated_over_shared"] = {
+            "requests": round(entry["isolated"]["requests"] / max(1, entry["shared"]["requests"]), 3),
+            "sequences": round(entry["isolated"]["sequences"] / max(1, entry["shared"]["sequences"]), 3),
+            "tokens_per_s": round(entry["isolated"]["tokens_per_s"] / max(1.0, entry["shared"]["tokens_per_s"]), 3)}
+        log(f"footprint M={M}: " + ", ".join(f"{k}: {entry[k]['sequences']} seqs "
+                                            f"{entry[k]['tokens_per_s'] / 1e6:.2f} M tok/s"
+                                            for k in ("isolated", "shared", "private")))
+        results.append(entry)
     line = {
-        "metric": "KV blocks and decode tokens/s: isolated stage pools with shared prompt blocks vs one "
-                  "engine with private copies (generator + fixer batches, one layer)",
-        "stages": per_stage,
-        "total_blocks_isolated": tot["blocks_isolated"], "total_blocks_private": tot["blocks_private"],
-        "footprint_ratio_private_over_isolated": round(tot["blocks_private"] / tot["blocks_isolated"], 3),
-        "admitted_batch_multiplier": round(tot["blocks_private"] / tot["blocks_isolated"], 3),
-        "tokens_per_s_isolated": round(tot["seqs"] / (tot["ms_isolated"] * 1e-3), 1),
-        "tokens_per_s_private": round(tot["seqs"] / (tot["ms_private"] * 1e-3), 1),
-        "note": "admitted_batch_multiplier: how many times more sequences of the same shapes the "
-                "private-copy footprint would hold under isolation (first order: block counts)",
-        "n_gpus": 1, "steps": args.steps, "data": "synthetic",
+        "metric": "sequences admitted and decode tokens/s of two engine replicas under a fixed KV "
+                  "budget per replica: isolated stage pools vs one shared engine vs no prefix sharing",
+        "budgets": results, "n_gpus": 1, "steps": args.steps, "data": "synthetic",
+        "note": "one layer; generator calls and fixer requests alternate in the demand; each "
+                "replica admits until a unit no longer fits; replicas are timed one at a time",
     }
     print(json.dumps(line), flush=True)
 
@@ -831,10 +1005,6 @@ def profile_loop(k, w, args):
     import torch
     from paper_2510_14126_amd import binding
     from paper_2510_14126_amd.device import PagedBatch
-    if args.stamp:
-        os.makedirs(os.path.dirname(os.path.abspath(args.stamp)), exist_ok=True)
-        with open(args.stamp, "w") as f:
-            json.dump(source_stamp(), f)
     S, kw = launch_configuration(k, w, args.partition_size, args.prefix_partition_size,
                                  args.cascade, args.groups)
     dev = torch.device("cuda:0")
@@ -906,7 +1076,7 @@ def main():
     ap.add_argument("--sq-kernel", default="cascade_kernel")
     ap.add_argument("--command-note", default="")
     ap.add_argument("--stamp", default=None,
-                    help="--profile-loop: write the source stamp here; ingest: the stamp to check")
+                    help="measuring runs: write the source stamp here; ingest: the stamp to check")
     ap.add_argument("--extend", action="store_true",
                     help="also time extend (chunked prefill) attention on --config k: each "
                          "sequence's tokens after its shared prompt as the chunk (the default run "
@@ -939,6 +1109,12 @@ def main():
         if args.ingest_stats:
             ingest_stats(args.ingest_stats, name, args.command_note, stamp, args.profile_name)
         return
+
+    if args.stamp:
+        # the sources this (profiled) run was built from, checked at ingest
+        os.makedirs(os.path.dirname(os.path.abspath(args.stamp)), exist_ok=True)
+        with open(args.stamp, "w") as f:
+            json.dump(source_stamp(), f)
 
     if args.footprint:
         run_footprint(args)

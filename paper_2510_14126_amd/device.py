@@ -31,6 +31,13 @@ class PagedBatch:
         self.partition_size = w.partition_size if partition_size is None else partition_size
         self.k = k_pool if k_pool is not None else _dev(w.k_pool, self.device)
         self.v = v_pool if v_pool is not None else _dev(w.v_pool, self.device)
+        # the library cannot see a device buffer's size: the pools must hold
+        # every block the handle will declare
+        need = w.num_blocks * w.num_kv_heads * 16 * w.head_dim
+        for name, t in (("k_pool", self.k), ("v_pool", self.v)):
+            if t.numel() < need or t.element_size() != 2:
+                raise ValueError(f"{name} holds {t.numel()} 16-bit values; {w.num_blocks} blocks "
+                                 f"of {w.num_kv_heads} x 16 x {w.head_dim} need {need}")
         self.q = _dev(w.q, self.device)
         self.bt = _dev(w.block_tables.astype(np.int32), self.device)
         self.ctx = _dev(w.context_lens.astype(np.int32), self.device)

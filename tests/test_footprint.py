@@ -40,3 +40,54 @@ def test_bench_launch_configurations():
     w = build_config(5, values=False)
     assert bench.launch_configuration(5, w)[1]["prefix_partition_size"] == 512
     assert bench.launch_configuration(5, w, cascade="off")[1] == {}
+
+
+def _nb(t):
+    return -(-t // 16)
+
+
+def test_deployments_under_a_fixed_kv_budget():
+    """Host accounting of the isolated / shared / private deployments: the
+    same total budget, whole requests (a generator call and a fixer request)
+    admitted in order, every replica within its budget, each stage's prompt
+    resident once per replica that serves the stage (referenced by every
+    sequence that maps it), exactly the blocks the sequences need; isolation
+    admits the most requests."""
+    from paper_2510_14126_amd import binding
+    from workloads import FIRST_ATTEMPT, stage_units
+    M = 1024
+    deps = bench.footprint_deployments(M, stage_units(7, 600))
+    requests = {}
+    for kind, reps in deps.items():
+        assert sum(r.budget for r in reps) == 2 * M
+        requests[kind] = sum(len(r.groups) for r in reps)
+        for r in reps:
+            assert r.blocks_used() <= r.budget
+            if not (r is deps["isolated"][0] or r is deps["isolated"][1]):
+                assert len(r.seqs["generator"]) == len(r.groups)    # one generator call per request
+            expect = r.prompt_blocks
+            for st, rows in r.seqs.items():
+                for ids, n in rows:
+                    assert len(ids) == _nb(n)
+                    assert len(set(ids)) == len(ids)
+                    if r.private:
+                        expect += _nb(n)
+                    else:
+                        expect += _nb(n) - 128 - (FIRST_ATTEMPT // 16 if st == "fixer" else 0)
+            if not r.private:
+                expect += len(r.groups) * (FIRST_ATTEMPT // 16)
+            assert r.blocks_used() == expect, kind
+            for st, ids in r.prompt.items():
+                assert binding.kv_pool_refcount(r.pool, ids[0]) == 1 + len(r.seqs[st])
+    gen, fix = deps["isolated"]
+    assert gen.prompt_blocks == 128 and fix.prompt_blocks == 128
+    assert all(r.prompt_blocks == 256 for r in deps["shared"])
+    assert all(r.prompt_blocks == 0 for r in deps["private"])
+    assert len(fix.seqs["generator"]) == 0 and len(gen.seqs["fixer"]) == 0
+    assert len(gen.seqs["generator"]) == len(fix.groups)           # the same requests
+    for r in deps["shared"] + deps["private"]:                      # both stages on each replica
+        assert len(r.seqs["generator"]) > 0 and len(r.seqs["fixer"]) > 0
+    assert requests["isolated"] >= requests["shared"] > requests["private"] > 0
+    for reps in deps.values():
+        for r in reps:
+            r.close()

@@ -472,3 +472,33 @@ def test_cascade_argmax_exact_slot(hq, where):
         assert np.all(got[:, 0] == pid % 256) and np.all(got[:, 1] == pid // 256) \
             and np.all(got[:, 2] == r), f"seq {b}: wanted slot ({pid},{r}), got {got[0]}"
         assert np.all(out[b, :, 3:] & 0x7FFF == 0)
+
+
+# ------------------------------------------------ batch-independent partials
+
+@pytest.mark.parametrize("S,lo,hi,B", [(128, 2000, 4500, 48), (512, 8000, 12000, 40),
+                                       (1024, 15000, 17000, 40)])
+def test_partials_do_not_depend_on_the_batch(S, lo, hi, B, oracle_pool):
+    """A sequence's split-KV partials have the same bits whether it is decoded
+    in a large batch (thousands of work items) or in a batch of three, and
+    the large batch passes the gate."""
+    from dataclasses import replace
+    rng = np.random.default_rng(160 + S)
+    ctx = rng.integers(lo, hi, size=B)
+    say(f"batch-independent partials S={S}: {B} sequences of {lo}..{hi} tokens, G = 8")
+    w = page_case(logical_case(160 + S, B, 64, 8, 128, ctx), 161, extra_blocks=7)
+    pb = run(w, S)
+    o, lse = pb.partials()
+    out = pb.out_bits()
+    pb.close()
+    assert_gate(out, oracle_pool.decode_workload(w)[0], f"large batch S={S}")
+    idx = [0, B // 2, B - 1]
+    sub = replace(w, batch=3, q=w.q[idx], block_tables=w.block_tables[idx],
+                  context_lens=w.context_lens[idx])
+    pb = run(sub, S)
+    o1, lse1 = pb.partials()
+    pb.close()
+    for i, b in enumerate(idx):
+        P = -(-int(w.context_lens[b]) // S)
+        assert np.array_equal(lse[b, :, :P], lse1[i, :, :P]), f"lse of sequence {b}"
+        assert np.array_equal(o[b, :, :P], o1[i, :, :P]), f"partials of sequence {b}"

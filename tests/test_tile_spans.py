@@ -18,7 +18,8 @@ def batch_of(w, S, prefix_len=0, pps=256, **kw):
     from paper_2510_14126_amd.device import PagedBatch
     if w.k_pool is None:                        # structure only: placeholder pools, never read
         w.q = np.zeros((w.batch, w.num_q_heads, w.head_dim), np.uint16)
-        dummy = torch.zeros(8, dtype=torch.int16)
+        n = w.num_blocks * w.num_kv_heads * 16 * w.head_dim
+        dummy = torch.zeros(1, dtype=torch.int16).expand(n)     # the pool's size, no storage
         kw.update(k_pool=dummy, v_pool=dummy)
     return PagedBatch(w, "cpu", partition_size=S, prefix_len=prefix_len,
                       prefix_partition_size=pps, **kw)

@@ -442,3 +442,45 @@ def duplicate_shared_blocks(w: Workload) -> Workload:
                     bt[b, j] = nxt; nxt += 1
     return replace(w, num_blocks=nb, block_tables=bt, k_pool=k, v_pool=v,
                    meta=dict(w.meta, duplicated=extra))
+
+
+# --------------------------------------------------------------------------
+# stage demand for the isolated-vs-shared footprint experiment
+# --------------------------------------------------------------------------
+
+GENERATOR_PROMPT = 2048    # schema prompt tokens of the SQL-generator stage
+FIXER_PROMPT = 2048        # schema prompt tokens of the SQL-error-fixer stage
+FIRST_ATTEMPT = 256        # a fixer request's failed first attempt, shared by its retries
+
+
+def stage_units(seed: int, n_units: int):
+    """Seeded demand of the two LLM stages as in configurations 2 and 3:
+    alternately a generator call (its tokens after the prompt: U[64, 512])
+    and a fixer request (1..5 retries, each U[128, 1024] tokens after the
+    prompt and the first attempt).  Returns [(stage, [suffix tokens, ...])]."""
+    rng = np.random.default_rng(seed)
+    units = []
+    for i in range(n_units):
+        if i % 2 == 0:
+            units.append(("generator", [int(rng.integers(64, 512, endpoint=True))]))
+        else:
+            r = int(rng.integers(1, 5, endpoint=True))
+            units.append(("fixer", [int(x) for x in rng.integers(128, 1024, size=r, endpoint=True)]))
+    return units
+
+
+def batch_from_tables(name: str, tables, context_lens, num_blocks: int, hq: int, hkv: int,
+                      d: int, seed: int, k_pool=None, v_pool=None, meta=None) -> Workload:
+    """A decode batch over given block tables: N(0,1) bf16 queries (and pools,
+    unless given) from seed."""
+    w = Workload(name=name, batch=len(tables), num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                 num_blocks=num_blocks, context_lens=np.asarray(context_lens, dtype=np.int32),
+                 block_tables=_tables_from_lists(tables), scale=1.0 / math.sqrt(d))
+    if k_pool is None:
+        shape = (num_blocks, hkv, BLOCK_SIZE, d)
+        k_pool = normal_bf16(shape, seed, STREAM_K)
+        v_pool = normal_bf16(shape, seed, STREAM_V)
+    w.k_pool, w.v_pool = k_pool, v_pool
+    w.q = normal_bf16((w.batch, hq, d), seed, STREAM_Q)
+    w.meta.update(meta or {})
+    return w
