@@ -596,7 +596,7 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
       *reinterpret_cast<uint32_t*>(orow + 2 * lane) = bf16_rne(o0 * inv) | (bf16_rne(o1 * inv) << 16);
     } else {
       const size_t row = ((size_t)b * p.num_q_heads + h0 + r) * p.part_stride + p.part_offset + part;
-      *reinterpret_cast<float2*>(p.part_o + row * kD + 2 * lane) = make_float2(o0 * inv, o1 * inv);
+      store_partial2(p.part_o + row * kD + 2 * lane, o0 * inv, o1 * inv);
       if (lane == 0)
         p.part_lse[row] = lt > 0.f ? (mx + log2f(lt)) * kLn2 : -__builtin_inff();
     }
@@ -776,7 +776,7 @@ __device__ __forceinline__ void shared_span_body(const PrefixParams& p, int g, c
           ((size_t)(sp.seq0 + R / G) * p.num_q_heads + g * G + R % G) * p.part_stride + part;
       float* po = p.part_o + row * kD + n;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) po[16 * j] = S.o[0][j][r] * f;
+      for (int j = 0; j < 8; ++j) store_partial(po + 16 * j, S.o[0][j][r] * f);
     }
   }
 }

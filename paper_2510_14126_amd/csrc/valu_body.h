@@ -405,9 +405,9 @@ __device__ __forceinline__ void decode_valu_body(const DecodeParams& p, int wg_i
       const size_t row = ((size_t)b * p.num_q_heads + h0 + r) * p.part_stride + p.part_offset + part;
       float* po = p.part_o + row * D;
       if constexpr (OPL == 2)
-        *reinterpret_cast<float2*>(po + 2 * lane) = make_float2(o[0] * inv, o[1] * inv);
+        store_partial2(po + 2 * lane, o[0] * inv, o[1] * inv);
       else
-        po[lane] = o[0] * inv;
+        store_partial(po + lane, o[0] * inv);
       if (lane == 0)
         p.part_lse[row] = lt > 0.f ? (mx + log2f(lt)) * kLn2 : -__builtin_inff();
     }
