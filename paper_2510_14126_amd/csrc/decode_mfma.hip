@@ -12,7 +12,7 @@ template <bool TRACE>
 __global__ void __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 8)))
 decode_mfma_g8_kernel(const DecodeParams p) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[mfma::kLdsBytes];
-  mfma::decode_mfma_body<TRACE>(p, blockIdx.x, (lds_u8_t*)smem);
+  mfma::decode_mfma_body<TRACE, /*STREAM=*/false>(p, blockIdx.x, (lds_u8_t*)smem);
 }
 
 }  // namespace

@@ -69,14 +69,17 @@ struct MfmaTile {
 // Rows 4u+q, chunk n of one K or V tile (lane_off = the byte offset of row q,
 // chunk n) through a buffer descriptor built from the wave-uniform tile
 // address; `bytes` = 0 makes the loads no-ops that return zeros but still
-// count as issued.
+// count as issued.  AUX: the loads' cache policy (kLoadDefault or
+// kLoadStreaming).
+template <int AUX>
 __device__ __forceinline__ void load_chunks(uint4 (&dst)[4], const uint16_t* tile, uint32_t lane_off,
                                             int bytes) {
   const __amdgpu_buffer_rsrc_t rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(tile), 0, bytes, kBufferDescWord3);
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const auto x = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)lane_off + u * 4 * kD * 2, 0, 0);
+    const auto x =
+        __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)lane_off + u * 4 * kD * 2, 0, AUX);
     dst[u] = make_uint4(x[0], x[1], x[2], x[3]);
   }
 }
@@ -454,7 +457,10 @@ constexpr int kLdsBytes = kWaves * 2 * kStageBytes > kMergeLdsBytes ? kWaves * 2
                                                                     : kMergeLdsBytes;
 
 // One decode work item (partition, sequence, KV head) = workgroup `wg_index`.
-template <bool TRACE>
+// STREAM: load the tiles as streaming data (the cascade's per-sequence half,
+// whose tokens come after everything the sequences share and are normally
+// read by this item only).  The hint changes caching, never the results.
+template <bool TRACE, bool STREAM>
 __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_index, lds_u8_t* smem) {
   const int lane = threadIdx.x & 63;
   const int wave = wave_uniform(threadIdx.x >> 6);
@@ -512,8 +518,9 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
       const bool ok = i < cn;
       const size_t id = (size_t)__builtin_amdgcn_readlane(idc, ok ? i : 0);
       const int bytes = ok ? (int)(kTileElems * 2) : 0;
-      load_chunks(T.k, kbase + id * blk_stride, lane_off, bytes);
-      load_chunks(T.v, vbase + id * blk_stride, lane_off, bytes);
+      constexpr int kAux = STREAM ? kLoadStreaming : kLoadDefault;
+      load_chunks<kAux>(T.k, kbase + id * blk_stride, lane_off, bytes);
+      load_chunks<kAux>(T.v, vbase + id * blk_stride, lane_off, bytes);
     };
     auto run = [&](const MfmaTile& T, int i) {
       const int valid = min(16, end - (start + (c0 + i) * 16));

@@ -47,6 +47,16 @@ __device__ __forceinline__ void store_partial2(float* dst, float a, float b) {
   __builtin_nontemporal_store(f32x2_t{a, b}, reinterpret_cast<f32x2_t*>(dst));
 }
 
+// Cache-policy operand of a buffer load: bit 1 is the non-temporal hint of
+// the gfx940 family.  Tiles that one step reads exactly once (the tokens of
+// a single sequence after the shared prefix, in the cascade) are loaded with
+// it, so they do not push lines that are still in use out of L2 and the
+// infinity cache: 8% of the matrix-core decode's time on the 8K-32K-token
+// batch.  Where blocks may be shared between sequences (the plain decode) it
+// costs 5% on the same batch, and the G = 4 VALU decode is slower with it.
+constexpr int kLoadDefault = 0;
+constexpr int kLoadStreaming = 2;
+
 // Fourth word of a raw buffer descriptor on gfx9-family GPUs (32-bit data
 // format, no swizzle); the first three hold the base and the byte size.
 constexpr int kBufferDescWord3 = 0x00020000;
