@@ -123,6 +123,11 @@ int kv_pool_num_free(const pa_kv_pool *pool, int32_t *n_out);
 /* Reference count of one block (0 = free). */
 int kv_pool_refcount(const pa_kv_pool *pool, int32_t id, int32_t *count_out);
 
+/* Number of blocks whose reference count is 2 or more (retained for a second
+ * table).  While it is 0 the decode kernels load every tile with a streaming
+ * cache hint (see paged_attn_decode). */
+int kv_pool_num_shared(const pa_kv_pool *pool, int64_t *n_out);
+
 /* Geometry: element strides of the pool [block][kv_head][token][dim], and
  * the bytes of one pool (K or V). */
 int kv_pool_layout(const pa_kv_pool *pool, int64_t elem_strides_out[4], int64_t *pool_bytes_out);
@@ -163,7 +168,12 @@ int paged_attn_workspace_size(int32_t batch, int32_t num_q_heads, int32_t head_d
  *   partial_out/_lse device fp32 partials (paged_attn_workspace_size), required
  *                    when there is more than one partition; the caller then
  *                    runs paged_attn_reduce on the same stream
- * G = 4 runs on VALU dot products, G = 8 on MFMA tiles. */
+ * G = 4 runs on VALU dot products, G = 8 on MFMA tiles.
+ * Cache policy: when the pool holds no shared block (kv_pool_num_shared is 0),
+ * no tile is read twice in a step and the kernels load the tiles with the
+ * non-temporal hint; otherwise with the default policy, so that blocks shared
+ * by several tables stay cached.  Tables that share blocks the allocator was
+ * not told about give the same results, only possibly slower. */
 int paged_attn_decode(const pa_kv_pool *pool, const void *q, const int32_t *block_tables,
                       int32_t bt_stride, const int32_t *context_lens, int32_t batch,
                       int32_t num_q_heads, float scale, int32_t max_context_len,
@@ -557,7 +567,9 @@ int pa_stream_copy(const void *src, void *dst, size_t bytes, void *stream);
  * grid a decode launch uses (one workgroup of four wavefronts per (span,
  * KV head), the head fastest, the span's 16-token blocks dealt round-robin
  * to the wavefronts, tiles_in_flight tiles of K and V in flight per
- * wavefront: 2 suits short spans, 4 long ones).  The
+ * wavefront: 2 suits short spans, 4 long ones), each tile read once, whole
+ * token rows per load instruction, with the streaming (non-temporal) cache
+ * hint, as the decode kernels read tiles that a step reads once.  The
  * time of one call over the tiles that a decode step reads is what that
  * access pattern costs on the memory system alone, the reference for the
  * decode kernels' own time.  Like pa_stream_copy it is a measurement helper

@@ -36,6 +36,7 @@ SIGNATURES = {
     "kv_pool_release": (_c_int, [_vp, _i32, _pi32]),
     "kv_pool_num_free": (_c_int, [_vp, _pi32]),
     "kv_pool_refcount": (_c_int, [_vp, _i32, _pi32]),
+    "kv_pool_num_shared": (_c_int, [_vp, _pi64]),
     "kv_pool_layout": (_c_int, [_vp, _pi64, _pi64]),
     "paged_attn_num_partitions": (_c_int, [_i32, _i32, _pi32]),
     "paged_attn_workspace_size": (_c_int, [_i32, _i32, _i32, _i32, _i32,
@@ -216,6 +217,12 @@ def kv_pool_num_free(pool: KVPool) -> int:
 def kv_pool_refcount(pool: KVPool, block_id: int) -> int:
     n = ctypes.c_int32()
     _check(_lib.kv_pool_refcount(pool._handle(), block_id, ctypes.byref(n)))
+    return n.value
+
+
+def kv_pool_num_shared(pool: KVPool) -> int:
+    n = ctypes.c_int64()
+    _check(_lib.kv_pool_num_shared(pool._handle(), ctypes.byref(n)))
     return n.value
 
 

@@ -20,6 +20,7 @@ struct pa_kv_pool {
   uint16_t* v;
   std::vector<int32_t> refcount;  // 0 = free
   std::vector<int32_t> free_stack; // top = back(); ids pop in ascending order initially
+  int64_t shared_blocks = 0;       // blocks whose reference count is 2 or more
 };
 
 namespace {
@@ -143,6 +144,9 @@ pa::DecodeParams decode_params(const DecodeArgs& a) {
   p.batch = a.batch;
   p.bt_stride = a.bt_stride;
   p.max_ctx = a.max_context_len;
+  // With no block shared by two tables every tile is read once per step:
+  // stream it past the caches.
+  p.stream_tiles = a.pool->shared_blocks == 0 ? 1 : 0;
   p.scale_log2 = a.scale * 1.4426950408889634f;
   return p;
 }
@@ -367,7 +371,8 @@ int kv_pool_retain(pa_kv_pool* pool, int32_t n, const int32_t* ids) {
     if (pool->refcount[ids[i]] == 0x7fffffff)
       return fail(PA_ESTATE, "kv_pool_retain: reference count of block %d overflows", ids[i]);
   }
-  for (int32_t i = 0; i < n; ++i) ++pool->refcount[ids[i]];
+  for (int32_t i = 0; i < n; ++i)
+    if (++pool->refcount[ids[i]] == 2) ++pool->shared_blocks;
   return PA_OK;
 }
 
@@ -380,7 +385,9 @@ int kv_pool_release(pa_kv_pool* pool, int32_t n, const int32_t* ids) {
       return fail(PA_ESTATE, "kv_pool_release: block %d released more often than retained", ids[i]);
   bool freed = false;
   for (int32_t i = 0; i < n; ++i) {
-    if (--pool->refcount[ids[i]] == 0) freed = true;
+    const int32_t left = --pool->refcount[ids[i]];
+    if (left == 0) freed = true;
+    if (left == 1) --pool->shared_blocks;
   }
   if (freed) rebuild_free(pool);
   return PA_OK;
@@ -389,6 +396,12 @@ int kv_pool_release(pa_kv_pool* pool, int32_t n, const int32_t* ids) {
 int kv_pool_num_free(const pa_kv_pool* pool, int32_t* n_out) {
   if (!pool || !n_out) return fail(PA_EINVAL, "kv_pool_num_free: NULL argument");
   *n_out = (int32_t)pool->free_stack.size();
+  return PA_OK;
+}
+
+int kv_pool_num_shared(const pa_kv_pool* pool, int64_t* n_out) {
+  if (!pool || !n_out) return fail(PA_EINVAL, "kv_pool_num_shared: NULL argument");
+  *n_out = pool->shared_blocks;
   return PA_OK;
 }
 

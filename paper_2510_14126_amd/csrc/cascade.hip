@@ -72,7 +72,7 @@ cascade_kernel(const PrefixParams pp, const DecodeParams dp, int prefix_runs, in
   }
   const int wg = idx * hkv + g;
   if constexpr (G == 4) {
-    valu::decode_valu_body<128, 4, PA_VALU_WAVES, kCascadeValuNbuf, TRACE>(dp, wg, lds);
+    valu::decode_valu_body<128, 4, PA_VALU_WAVES, kCascadeValuNbuf, TRACE, /*STREAM=*/true>(dp, wg, lds);
   } else {
     mfma::decode_mfma_body<TRACE, /*STREAM=*/true>(dp, wg, lds);
   }

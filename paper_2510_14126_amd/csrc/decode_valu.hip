@@ -5,21 +5,26 @@
 namespace pa {
 namespace {
 
-template <int D, int G, int W, int NBUF, bool TRACE>
+template <int D, int G, int W, int NBUF, bool TRACE, bool STREAM>
 __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(PA_VALU_MIN_WAVES, 8)))
 decode_valu_kernel(const DecodeParams p) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[valu::valu_lds_bytes<D, G, W>()];
-  valu::decode_valu_body<D, G, W, NBUF, TRACE>(p, blockIdx.x, (lds_u8_t*)smem);
+  valu::decode_valu_body<D, G, W, NBUF, TRACE, STREAM>(p, blockIdx.x, (lds_u8_t*)smem);
 }
 
+// The trace kernels keep the default cache policy (the hint changes no index).
 template <int D, int G, bool TRACE>
 hipError_t launch_t(const DecodeParams& p, hipStream_t stream) {
   constexpr int W = PA_VALU_WAVES;
   constexpr int NBUF = PA_VALU_NBUF;
   const int64_t grid = decode_items(p) * p.num_kv_heads;
   if (grid == 0) return hipSuccess;
-  hipLaunchKernelGGL((decode_valu_kernel<D, G, W, NBUF, TRACE>), dim3((unsigned)grid),
-                     dim3(64 * W), 0, stream, p);
+  if (!TRACE && p.stream_tiles)
+    hipLaunchKernelGGL((decode_valu_kernel<D, G, W, NBUF, TRACE, !TRACE>), dim3((unsigned)grid),
+                       dim3(64 * W), 0, stream, p);
+  else
+    hipLaunchKernelGGL((decode_valu_kernel<D, G, W, NBUF, TRACE, false>), dim3((unsigned)grid),
+                       dim3(64 * W), 0, stream, p);
   return hipGetLastError();
 }
 

@@ -5,8 +5,11 @@
 // blocks round-robin through a ring that keeps NIF tiles of K and V in flight
 // each (two suit short spans, where deeper rings only lengthen the memory
 // queues; four suit long ones), and fold every 32-bit word they read with XOR so that no load
-// is dead.  The time of one launch over the tiles a decode step reads is
-// what that access pattern costs on the memory system alone.
+// is dead.  Every tile is read once, 1 KiB of contiguous rows per load
+// instruction, with the streaming cache hint (kLoadStreaming), like the
+// tiles a decode step reads once.  The time of one launch over the tiles a
+// decode step reads is what that access pattern costs on the memory system
+// alone.
 #include "kernels.h"
 #include "pa_device.h"
 
@@ -65,8 +68,8 @@ gather_tiles_kernel(const uint16_t* __restrict__ kp, const uint16_t* __restrict_
           const_cast<uint8_t*>(vbase + id * blk_stride), 0, bytes, kBufferDescWord3);
 #pragma unroll
       for (int u = 0; u < kPerLane; ++u) {
-        const auto k = __builtin_amdgcn_raw_buffer_load_b128(rk, (u * 64 + lane) * 16, 0, 0);
-        const auto v = __builtin_amdgcn_raw_buffer_load_b128(rv, (u * 64 + lane) * 16, 0, 0);
+        const auto k = __builtin_amdgcn_raw_buffer_load_b128(rk, (u * 64 + lane) * 16, 0, kLoadStreaming);
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(rv, (u * 64 + lane) * 16, 0, kLoadStreaming);
         dst[0][u] = make_uint4(k[0], k[1], k[2], k[3]);
         dst[1][u] = make_uint4(v[0], v[1], v[2], v[3]);
       }

@@ -36,6 +36,7 @@ struct DecodeParams {
   int32_t item_order;            // workgroup -> work item order (decode_item)
   const int32_t* items;          // optional work list: item = part * batch + b, or NULL
   int32_t num_items;             // entries of items
+  int32_t stream_tiles;          // 1: load the tiles with the streaming cache hint (plain decode)
   float scale_log2;              // softmax scale * log2(e)
 };
 

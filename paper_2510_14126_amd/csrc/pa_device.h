@@ -48,12 +48,15 @@ __device__ __forceinline__ void store_partial2(float* dst, float a, float b) {
 }
 
 // Cache-policy operand of a buffer load: bit 1 is the non-temporal hint of
-// the gfx940 family.  Tiles that one step reads exactly once (the tokens of
-// a single sequence after the shared prefix, in the cascade) are loaded with
-// it, so they do not push lines that are still in use out of L2 and the
-// infinity cache: 8% of the matrix-core decode's time on the 8K-32K-token
-// batch.  Where blocks may be shared between sequences (the plain decode) it
-// costs 5% on the same batch, and the G = 4 VALU decode is slower with it.
+// the gfx940 family.  Tiles that one step reads exactly once (a sequence's
+// tokens after what the batch shares, in the cascade; every tile when the
+// pool holds no shared block) are loaded with it, so they do not push lines
+// that are still in use out of L2 and the infinity cache: 8-11% of the
+// decode time on the long-context and shared-pool batches.  A line must be
+// read whole by one instruction: one read in parts by several instructions
+// can be evicted between them and fetched again.  Where blocks are shared
+// between sequences the plain decode keeps the default (the hint cost 5%
+// there on the long-context batch).
 constexpr int kLoadDefault = 0;
 constexpr int kLoadStreaming = 2;
 

@@ -19,9 +19,12 @@
 //    its dims; a DPP reduce-scatter across the 16 lanes of the row (ror 8,
 //    half-mirror, quad xor 2, quad xor 1) leaves in lane (J, c) the score of
 //    query row c/4 (+4k) for token 4 tg(c) + J, tg(c) = (c%4) ^ 3*bit2(c).
-//    The reduce-scatter needs no lane-dependent selects: each lane loads its
+//    The reduce-scatter needs no lane-dependent selects: each lane holds its
 //    query rows and its K row quads in a lane-dependent order (row r ^ c/4,
 //    quad u ^ tg(c)), so every level keeps the same slots on both partners.
+//    The query rows are loaded in that order; K is loaded in row order, so
+//    that every load instruction reads whole token rows, and its quads are
+//    put in order by selects in registers (two conditional swaps).
 //  * PV: lane (J, c) accumulates its dims over tokens = J mod 4, two tokens
 //    per v_dot2c_f32_bf16: each probability is split into a bf16 high part
 //    and the bf16-rounded remainder (about 2^-17 relative together; the row
@@ -72,7 +75,7 @@ __device__ __forceinline__ void static_for(F&& f) {
 template <int D>
 struct KvTile {
   static constexpr int VW = D / 32;   // dwords per lane per token (4: 16 B, 2: 8 B)
-  uint32_t k[4][VW];                  // token 4(u ^ tg(c)) + J, dims (D/16)*c ..
+  uint32_t k[4][VW];                  // token 4u + J, dims (D/16)*c ..
   uint32_t v[4][VW];                  // token 4u + J, dims (D/16)*c ..
 };
 
@@ -90,7 +93,8 @@ constexpr int pair_pos() { return 4 * R4 + ((R4 & 1) ? 2 - 2 * H : 2 * H); }
 // address math, and the descriptor bounds every access to the tile.
 // `bytes` = 0 turns the loads into no-ops that return zeros but still count
 // as issued, so every path through the prefetch ring issues the same loads.
-template <int D>
+// AUX: the loads' cache policy (kLoadDefault or kLoadStreaming).
+template <int D, int AUX>
 __device__ __forceinline__ void load_rows(uint32_t (&dst)[4][D / 32], const uint16_t* tile,
                                           const uint32_t (&lane_off)[4], int bytes) {
   const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
@@ -99,10 +103,10 @@ __device__ __forceinline__ void load_rows(uint32_t (&dst)[4][D / 32], const uint
   for (int u = 0; u < 4; ++u) {
     const int off = (int)lane_off[u];
     if constexpr (D == 128) {
-      const auto x = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, 0);
+      const auto x = __builtin_amdgcn_raw_buffer_load_b128(rsrc, off, 0, AUX);
       dst[u][0] = x[0]; dst[u][1] = x[1]; dst[u][2] = x[2]; dst[u][3] = x[3];
     } else {
-      const auto x = __builtin_amdgcn_raw_buffer_load_b64(rsrc, off, 0, 0);
+      const auto x = __builtin_amdgcn_raw_buffer_load_b64(rsrc, off, 0, AUX);
       dst[u][0] = x[0]; dst[u][1] = x[1];
     }
   }
@@ -126,6 +130,23 @@ __device__ __forceinline__ void process_tile(WaveState<D, G>& S, const KvTile<D>
   constexpr int VW = D / 32;
   constexpr int DPL = D / 16;
 
+  // K quads in reduce-scatter order: slot u takes row quad u ^ tg(c), by a
+  // conditional swap on each bit of tg(c).
+  uint32_t kq[4][VW];
+  {
+    const int t = token_quad(c);
+    const bool s1 = (t & 1) != 0, s2 = (t & 2) != 0;
+#pragma unroll
+    for (int w = 0; w < VW; ++w) {
+      const uint32_t a0 = s1 ? T.k[1][w] : T.k[0][w], a1 = s1 ? T.k[0][w] : T.k[1][w];
+      const uint32_t a2 = s1 ? T.k[3][w] : T.k[2][w], a3 = s1 ? T.k[2][w] : T.k[3][w];
+      kq[0][w] = s2 ? a2 : a0;
+      kq[1][w] = s2 ? a3 : a1;
+      kq[2][w] = s2 ? a0 : a2;
+      kq[3][w] = s2 ? a1 : a3;
+    }
+  }
+
   // Partial scores over this lane's dims, ordered so the reduce-scatter hands
   // lane c the values (row c/4 + 4k, token quad c%4) in slot k.
   float y[4 * G];
@@ -135,7 +156,7 @@ __device__ __forceinline__ void process_tile(WaveState<D, G>& S, const KvTile<D>
     for (int u = 0; u < 4; ++u) {
       float a = 0.f;
 #pragma unroll
-      for (int w = 0; w < VW; ++w) a = dot2_bf16(qv[r][w], T.k[u][w], a);
+      for (int w = 0; w < VW; ++w) a = dot2_bf16(qv[r][w], kq[u][w], a);
       y[R * (4 * (r % 4) + u) + r / 4] = a;
     }
   row_reduce_scatter16(y);
@@ -218,8 +239,10 @@ template <int D, int G, int W>
 constexpr int valu_lds_bytes() { return (2 * W * G + W * 4 * G * D) * 4; }
 
 // One work item (partition, sequence, KV head) = workgroup `wg_index`;
-// `smem` points at valu_lds_bytes<D, G, W>() bytes of LDS.
-template <int D, int G, int W, int NBUF, bool TRACE>
+// `smem` points at valu_lds_bytes<D, G, W>() bytes of LDS.  STREAM: load the
+// tiles as streaming data (kLoadStreaming); it changes caching, never the
+// results.
+template <int D, int G, int W, int NBUF, bool TRACE, bool STREAM>
 __device__ __forceinline__ void decode_valu_body(const DecodeParams& p, int wg_index, lds_u8_t* smem) {
   constexpr int R = G / 4;
   constexpr int DPL = D / 16;
@@ -280,14 +303,10 @@ __device__ __forceinline__ void decode_valu_body(const DecodeParams& p, int wg_i
   const uint16_t* kbase = p.k_pool + (size_t)g * kTileElems;
   const uint16_t* vbase = p.v_pool + (size_t)g * kTileElems;
   const size_t item = ((size_t)part * p.batch + b) * p.num_kv_heads + g;
-  // Byte offsets of the lane's slice in row quad u: V in quad order, K in
-  // the order the reduce-scatter needs.
-  uint32_t voff[4], koff[4];
+  // Byte offsets of the lane's slice in row quad u (K and V alike).
+  uint32_t roff[4];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    voff[u] = (uint32_t)((4 * u + grp) * D + (D / 16) * tok) * 2u;
-    koff[u] = (uint32_t)((4 * (u ^ token_quad(tok)) + grp) * D + (D / 16) * tok) * 2u;
-  }
+  for (int u = 0; u < 4; ++u) roff[u] = (uint32_t)((4 * u + grp) * D + (D / 16) * tok) * 2u;
 
   for (int c0 = 0; c0 < nblk; c0 += 64) {
     const int cn = min(64, nblk - c0);
@@ -299,8 +318,9 @@ __device__ __forceinline__ void decode_valu_body(const DecodeParams& p, int wg_i
       const bool ok = i < cn;
       const size_t id = (size_t)__builtin_amdgcn_readlane(idc, ok ? i : 0);
       const int bytes = ok ? 16 * D * 2 : 0;
-      load_rows<D>(T.k, kbase + id * blk_stride, koff, bytes);
-      load_rows<D>(T.v, vbase + id * blk_stride, voff, bytes);
+      constexpr int kAux = STREAM ? kLoadStreaming : kLoadDefault;
+      load_rows<D, kAux>(T.k, kbase + id * blk_stride, roff, bytes);
+      load_rows<D, kAux>(T.v, vbase + id * blk_stride, roff, bytes);
     };
     auto run = [&](const KvTile<D>& T, int i) {
       const int valid = min(16, end - (start + (c0 + i) * 16));

@@ -77,6 +77,9 @@ static void allocator(std::mt19937& rng) {
       int32_t c = -1;
       CHECK(kv_pool_refcount(p, i, &c) == PA_OK && c == count[i]);
     }
+    int64_t shared = -1, expect = 0;
+    for (int32_t i = 0; i < 64; ++i) expect += count[i] >= 2;
+    CHECK(kv_pool_num_shared(p, &shared) == PA_OK && shared == expect);
   }
   int64_t strides[4], bytes = 0;
   CHECK(kv_pool_layout(p, strides, &bytes) == PA_OK && bytes == 64LL * 8 * 16 * 128 * 2);

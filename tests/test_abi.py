@@ -27,7 +27,7 @@ def declared_functions():
 
 def test_header_and_library_agree():
     names = declared_functions()
-    assert len(names) == 34, names
+    assert len(names) == 35, names
     lib = pa.library()
     for n in names:
         assert hasattr(lib, n), f"library does not export {n}"
@@ -82,11 +82,42 @@ def test_shared_prefix_refcounts():
     pa.kv_pool_retain(p, prefix)          # a second sequence maps the prefix
     pa.kv_pool_retain(p, prefix)          # and a third
     assert [pa.kv_pool_refcount(p, i) for i in prefix] == [3, 3, 3]
+    assert pa.kv_pool_num_shared(p) == 3
     pa.kv_pool_release(p, prefix)
+    assert pa.kv_pool_num_shared(p) == 3
     pa.kv_pool_release(p, prefix)
     assert pa.kv_pool_num_free(p) == 5    # still held by the first sequence
+    assert pa.kv_pool_num_shared(p) == 0
     pa.kv_pool_release(p, prefix)
     assert pa.kv_pool_num_free(p) == 8
+
+
+def test_shared_block_count_follows_every_change():
+    # Randomised retain/release sequences (repeated ids in one call included)
+    # against a host model of the reference counts.
+    import random
+    rng = random.Random(7)
+    p = make_pool(nb=12)
+    ids = pa.kv_pool_alloc(p, 12)
+    model = {i: 1 for i in ids}
+    for _ in range(300):
+        pick = [rng.choice(ids) for _ in range(rng.randint(1, 4))]
+        if rng.random() < 0.55:
+            if all(model[i] > 0 for i in pick):
+                pa.kv_pool_retain(p, pick)
+                for i in pick:
+                    model[i] += 1
+        else:
+            need = {i: pick.count(i) for i in pick}
+            if all(model[i] >= c for i, c in need.items()):
+                pa.kv_pool_release(p, pick)
+                for i in pick:
+                    model[i] -= 1
+            else:
+                with pytest.raises(pa.PagedAttnError):
+                    pa.kv_pool_release(p, pick)
+        assert pa.kv_pool_num_shared(p) == sum(1 for c in model.values() if c >= 2)
+        assert [pa.kv_pool_refcount(p, i) for i in ids] == [model[i] for i in ids]
 
 
 def test_state_violations_change_nothing():
