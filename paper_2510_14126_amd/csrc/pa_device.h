@@ -38,13 +38,18 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Split-KV partial rows are written once by the decode and read once by the
-// reduce kernel.  Non-temporal stores stream them out of L2 ahead of the KV
-// tiles that the decode is still reading (about 1.5% of the decode time on
-// the 8K-32K-token batch, where partials are 2% of the bytes moved).
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ void store_partial(float* dst, float a) { __builtin_nontemporal_store(a, dst); }
+// reduce kernel.  They are stored with device scope (relaxed atomic stores at
+// agent scope: plain vector stores with the sc1 bit), which writes them
+// through L2 instead of leaving dirty lines among the KV tiles that the
+// decode is still reading.  On the 8K-32K-token batch, where partials are 2%
+// of the bytes moved, the decode measured 1.6% faster than with non-temporal
+// stores and 8% faster than with default (write-back) stores.
+__device__ __forceinline__ void store_partial(float* dst, float a) {
+  __hip_atomic_store(dst, a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 __device__ __forceinline__ void store_partial2(float* dst, float a, float b) {
-  __builtin_nontemporal_store(f32x2_t{a, b}, reinterpret_cast<f32x2_t*>(dst));
+  const uint64_t v = ((uint64_t)__float_as_uint(b) << 32) | __float_as_uint(a);
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(dst), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Cache-policy operand of a buffer load: bit 1 is the non-temporal hint of
