@@ -252,6 +252,34 @@ def test_shared_prefix_equals_duplicated_bit_identical(hq):
     assert np.array_equal(a, b)
 
 
+@pytest.mark.parametrize("S", [0, 512])
+@pytest.mark.parametrize("hq", [32, 64])
+def test_cache_policy_changes_no_bit(hq, S):
+    """The plain decode loads its tiles with the streaming hint while the pool
+    holds no shared block and with the default policy otherwise: one extra
+    reference to a block switches the policy, never a result."""
+    say(f"cache policy switch Hq={hq} S={S}")
+    from paper_2510_14126_amd import binding
+    from paper_2510_14126_amd.device import PagedBatch
+    w = page_case(logical_case(34, 6, hq, 8, 128, [900, 40, 600, 33, 2048, 1500]), 8)
+    pb = PagedBatch(w, DEV, partition_size=S)
+    assert binding.kv_pool_num_shared(pb.pool) == 0
+    pb.run()
+    torch.cuda.synchronize()
+    streamed = pb.out_bits().copy()
+    some_block = int(w.block_tables[0, 0])
+    binding.kv_pool_retain(pb.pool, [some_block])
+    assert binding.kv_pool_num_shared(pb.pool) == 1
+    pb.out.zero_()
+    pb.run()
+    torch.cuda.synchronize()
+    cached = pb.out_bits().copy()
+    binding.kv_pool_release(pb.pool, [some_block])
+    pb.close()
+    assert np.array_equal(streamed, cached)
+    assert_gate(streamed, decode_workload(w)[0], f"cache policy Hq={hq} S={S}")
+
+
 @pytest.mark.parametrize("k", [2, 1])
 def test_repeat_runs_bit_identical(k, stage_batches):
     say(f"determinism config {k}")
