@@ -9,6 +9,7 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 from oracle import compare, extend_attention, paged_decode  # noqa: E402
+from oracle.attention import bf16_to_f64  # noqa: E402
 from workloads import f32_to_bf16_bits, logical_case, page_case  # noqa: E402
 
 DEV = "cuda:0"
@@ -171,3 +172,52 @@ def test_extend_bench_batches_all_rows(k, stage_batches, oracle_pool):
     rep = compare(out, ref)
     say(f"extend bench batch config {k}, all rows: {rep}")
     assert rep.passed, f"config {k}: {rep}"
+
+
+def _extend_argmax(ctx, chunk, targets, hq):
+    """Every chunk row's query is e0; K of one cached target token is 4096 e0
+    and K of each sequence's last token 8192 e0, every other used slot K = 0;
+    V encodes the physical slot (block mod 256, block div 256, row) as exact
+    bf16 integers.  Rows past the context and unused blocks hold K = 8192 e0
+    and V = NaN.  So chunk row i must return exactly V[target] if it does
+    not see the last token (i < L - 1, causal mask) and V[last] if it does."""
+    w, q, q_start = make_extend(77, ctx, chunk, hq=hq, poison=True)
+    e0 = np.zeros(128, np.float32)
+    e0[0] = 1.0
+    q[:] = f32_to_bf16_bits(e0)
+    nblk = (w.context_lens + 15) // 16
+    used = {(int(w.block_tables[b, j]), r) for b in range(w.batch) for j in range(nblk[b])
+            for r in range(min(16, int(w.context_lens[b]) - 16 * j))}
+    for (pid, r) in used:
+        w.k_pool[pid, :, r, :] = 0
+        w.v_pool[pid, :, r, :] = 0
+        w.v_pool[pid, :, r, 0:3] = f32_to_bf16_bits(np.float32([pid % 256, pid // 256, r]))
+    want = []
+    for b, t in enumerate(targets):
+        n, L = int(ctx[b]), int(chunk[b])
+        assert t < n - L, "the target lies in the cached context, seen by every chunk row"
+        slot_t = (int(w.block_tables[b, t // 16]), t % 16)
+        slot_l = (int(w.block_tables[b, (n - 1) // 16]), (n - 1) % 16)
+        w.k_pool[slot_t[0], :, slot_t[1], 0] = 0x4580   # 4096.0
+        w.k_pool[slot_l[0], :, slot_l[1], 0] = 0x4600   # 8192.0
+        want.append((slot_t, slot_l))
+    return w, q, q_start, want
+
+
+@pytest.mark.parametrize("hq", [32, 64], ids=["g4", "g8"])
+def test_extend_argmax_reads_exact_slot_and_causal_mask(hq):
+    ctx = [40, 513, 1024, 4100, 8192]
+    chunk = [1, 17, 512, 1000, 2048]
+    targets = [16, 495, 0, 3099, 4096]
+    say(f"extend argmax slot selection and causal mask Hq={hq}")
+    w, q, q_start, want = _extend_argmax(ctx, chunk, targets, hq)
+    out = gpu_extend(w, q, q_start)
+    for b, (slot_t, slot_l) in enumerate(want):
+        rows = out[q_start[b]:q_start[b + 1]]
+        codes = np.stack([np.asarray([s[0] % 256, s[0] // 256, s[1]], np.float64)
+                          for s in (slot_t, slot_l)])
+        got = bf16_to_f64(rows[:, :, :3])
+        L = rows.shape[0]
+        assert np.all(got[:L - 1] == codes[0]), f"seq {b}: rows before the last must read {slot_t}"
+        assert np.all(got[L - 1] == codes[1]), f"seq {b}: the last row must read {slot_l}"
+        assert np.all(rows[:, :, 3:] & 0x7FFF == 0)
