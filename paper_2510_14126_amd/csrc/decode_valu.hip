@@ -19,12 +19,15 @@ hipError_t launch_t(const DecodeParams& p, hipStream_t stream) {
   constexpr int NBUF = PA_VALU_NBUF;
   const int64_t grid = decode_items(p) * p.num_kv_heads;
   if (grid == 0) return hipSuccess;
-  if (!TRACE && p.stream_tiles)
-    hipLaunchKernelGGL((decode_valu_kernel<D, G, W, NBUF, TRACE, !TRACE>), dim3((unsigned)grid),
-                       dim3(64 * W), 0, stream, p);
-  else
-    hipLaunchKernelGGL((decode_valu_kernel<D, G, W, NBUF, TRACE, false>), dim3((unsigned)grid),
-                       dim3(64 * W), 0, stream, p);
+  if constexpr (!TRACE) {
+    if (p.stream_tiles) {
+      hipLaunchKernelGGL((decode_valu_kernel<D, G, W, NBUF, false, true>), dim3((unsigned)grid),
+                         dim3(64 * W), 0, stream, p);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL((decode_valu_kernel<D, G, W, NBUF, TRACE, false>), dim3((unsigned)grid),
+                     dim3(64 * W), 0, stream, p);
   return hipGetLastError();
 }
 
