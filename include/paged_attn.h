@@ -201,7 +201,10 @@ int paged_attn_reduce(const float *partial_out, const float *partial_lse,
  * that prefix once per KV head for all B*G query rows together, as dense
  * matrix-core tiles, and over each sequence's remaining tokens with the
  * per-sequence kernels; paged_attn_reduce_cascade merges both kinds of
- * partials by log-sum-exp into the same result as paged_attn_decode.
+ * partials by log-sum-exp into the same result as paged_attn_decode.  The
+ * per-sequence part loads its tiles (the tokens after everything the batch
+ * or a group shares) with the non-temporal cache hint, whatever the pool's
+ * reference counts; the shared parts keep the default policy.
  * ------------------------------------------------------------------------- */
 
 /* Partial-buffer sizes of a cascade step and the partition count per
