@@ -518,6 +518,41 @@ int paged_attn_append_kv(const pa_kv_pool *pool, const void *k_new, const void *
                          const int32_t *block_tables, int32_t bt_stride,
                          const int32_t *context_lens, int32_t batch, void *stream);
 
+/* Append and decode in one launch: the same pools, outputs and partials as
+ * paged_attn_append_kv followed by paged_attn_decode (items = NULL) or
+ * paged_attn_decode_scheduled (a work list from paged_attn_schedule), bit
+ * for bit, with one kernel launch less per decode step.  The work item that
+ * holds token n-1 of sequence b (n = context_lens[b] >= 1, clamped into
+ * [0, max_context_len] like the decode's lengths) uses k_new[b] / v_new[b]
+ * for that token whatever the pool slot holds, and writes them into the slot
+ * for later steps.  The slot's block must belong to sequence b alone, as for
+ * paged_attn_append_kv.
+ *   k_new, v_new  device bf16 [batch][num_kv_heads][head_dim], 16-byte aligned
+ * Other arguments as in paged_attn_decode_scheduled. */
+int paged_attn_decode_append(const pa_kv_pool *pool, const void *q, const void *k_new,
+                             const void *v_new, const int32_t *block_tables, int32_t bt_stride,
+                             const int32_t *context_lens, int32_t batch, int32_t num_q_heads,
+                             float scale, int32_t max_context_len, int32_t partition_size,
+                             const int32_t *items, int32_t num_items, void *out,
+                             float *partial_out, float *partial_lse, void *stream);
+
+/* The same for a cascade step: paged_attn_append_kv followed by
+ * paged_attn_decode_cascade_groups (group_len > 0), or by
+ * paged_attn_decode_cascade / _scheduled (group_len 0: group_start and
+ * num_groups are ignored); items may be NULL.  The new token must come after
+ * everything the batch or its group shares (n - 1 >= prefix_len + group_len):
+ * its row is appended by the per-sequence part of the launch only.  Follow
+ * with the matching paged_attn_reduce_cascade* call on the same stream. */
+int paged_attn_decode_cascade_append(const pa_kv_pool *pool, const void *q, const void *k_new,
+                                     const void *v_new, const int32_t *block_tables,
+                                     int32_t bt_stride, const int32_t *context_lens, int32_t batch,
+                                     int32_t num_q_heads, float scale, int32_t max_context_len,
+                                     int32_t partition_size, int32_t prefix_len,
+                                     int32_t prefix_partition_size, const int32_t *group_start,
+                                     int32_t num_groups, int32_t max_group_size, int32_t group_len,
+                                     const int32_t *items, int32_t num_items, float *partial_out,
+                                     float *partial_lse, void *stream);
+
 /* ---------------------------------------------------------------------------
  * Extend (chunked prefill) attention.
  *

@@ -58,6 +58,11 @@ SIGNATURES = {
                                                   _vp, _vp, _vp]),
     "paged_attn_reduce_cascade_groups": (_c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32,
                                                   _i32, _i32, _vp, _vp]),
+    "paged_attn_decode_append": (_c_int, [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32,
+                                          _i32, _vp, _i32, _vp, _vp, _vp, _vp]),
+    "paged_attn_decode_cascade_append": (_c_int, [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32,
+                                                  _i32, _i32, _i32, _i32, _vp, _i32, _i32, _i32, _vp,
+                                                  _i32, _vp, _vp, _vp]),
     "paged_attn_decode_scheduled": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32, _i32,
                                              _vp, _i32, _vp, _vp, _vp, _vp]),
     "paged_attn_decode_cascade_scheduled": (_c_int, [_vp, _vp, _vp, _i32, _vp, _i32, _i32, _f32, _i32,
@@ -288,6 +293,27 @@ def paged_attn_append_kv(pool: KVPool, k_new, v_new, block_tables, bt_stride, co
                          stream=None) -> None:
     _check(_lib.paged_attn_append_kv(pool._handle(), _ptr(k_new), _ptr(v_new), _ptr(block_tables),
                                      bt_stride, _ptr(context_lens), batch, _ptr(stream)))
+
+
+def paged_attn_decode_append(pool: KVPool, q, k_new, v_new, block_tables, bt_stride, context_lens,
+                             batch, num_q_heads, scale, max_context_len, partition_size, items,
+                             num_items, out, partial_out=None, partial_lse=None, stream=None) -> None:
+    _check(_lib.paged_attn_decode_append(
+        pool._handle(), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(block_tables), bt_stride,
+        _ptr(context_lens), batch, num_q_heads, scale, max_context_len, partition_size, _ptr(items),
+        num_items, _ptr(out), _ptr(partial_out), _ptr(partial_lse), _ptr(stream)))
+
+
+def paged_attn_decode_cascade_append(pool: KVPool, q, k_new, v_new, block_tables, bt_stride,
+                                     context_lens, batch, num_q_heads, scale, max_context_len,
+                                     partition_size, prefix_len, prefix_partition_size, group_start,
+                                     num_groups, max_group_size, group_len, items, num_items,
+                                     partial_out, partial_lse, stream=None) -> None:
+    _check(_lib.paged_attn_decode_cascade_append(
+        pool._handle(), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(block_tables), bt_stride,
+        _ptr(context_lens), batch, num_q_heads, scale, max_context_len, partition_size, prefix_len,
+        prefix_partition_size, _ptr(group_start), num_groups, max_group_size, group_len, _ptr(items),
+        num_items, _ptr(partial_out), _ptr(partial_lse), _ptr(stream)))
 
 
 def paged_attn_cascade_workspace_size(batch, num_q_heads, head_dim, max_context_len,

@@ -95,6 +95,8 @@ struct DecodeArgs {
   int32_t num_q_heads;
   float scale;
   int32_t max_context_len;
+  const void* k_new = nullptr;     // fused KV append: [batch][num_kv_heads][head_dim] bf16, or NULL
+  const void* v_new = nullptr;
 };
 
 // Checks shared by every decode entry point; fills the group size.
@@ -121,6 +123,10 @@ int validate_decode(const DecodeArgs& a, int32_t* group, const char* fn) {
   if (!aligned(a.q, 16)) return fail(PA_EINVAL, "%s: q is not 16-byte aligned", fn);
   if (!aligned(a.block_tables, 4) || !aligned(a.context_lens, 4))
     return fail(PA_EINVAL, "%s: block_tables/context_lens are not 4-byte aligned", fn);
+  if ((a.k_new != nullptr) != (a.v_new != nullptr))
+    return fail(PA_EINVAL, "%s: k_new and v_new must both be given or both be NULL", fn);
+  if (a.k_new && (!aligned(a.k_new, 16) || !aligned(a.v_new, 16)))
+    return fail(PA_EINVAL, "%s: k_new/v_new are not 16-byte aligned", fn);
   return PA_OK;
 }
 
@@ -148,6 +154,12 @@ pa::DecodeParams decode_params(const DecodeArgs& a) {
   // stream it past the caches.
   p.stream_tiles = a.pool->shared_blocks == 0 ? 1 : 0;
   p.scale_log2 = a.scale * 1.4426950408889634f;
+  if (a.k_new) {
+    p.k_new = static_cast<const uint16_t*>(a.k_new);
+    p.v_new = static_cast<const uint16_t*>(a.v_new);
+    p.k_pool_w = a.pool->k;
+    p.v_pool_w = a.pool->v;
+  }
   return p;
 }
 
@@ -530,9 +542,10 @@ int cascade_impl(const pa_kv_pool* pool, const void* q, const int32_t* block_tab
                  bool scheduled, const int32_t* items, int32_t num_items,
                  const int32_t* group_start = nullptr, int32_t num_groups = 0,
                  int32_t max_group_size = 0, int32_t group_len = 0, int32_t* trace = nullptr,
-                 int64_t trace_capacity = 0, bool tracing = false) {
+                 int64_t trace_capacity = 0, bool tracing = false, const void* k_new = nullptr,
+                 const void* v_new = nullptr) {
   const DecodeArgs a{pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
-                     max_context_len};
+                     max_context_len, k_new, v_new};
   int32_t group = 0;
   int rc = validate_decode(a, &group, fn);
   if (rc) return rc;
@@ -684,6 +697,39 @@ int paged_attn_decode_cascade_groups(const pa_kv_pool* pool, const void* q,
                       max_context_len, partition_size, prefix_len, prefix_partition_size,
                       partial_out, partial_lse, stream, fn, items != nullptr, items, num_items,
                       group_start, num_groups, max_group_size, group_len);
+}
+
+int paged_attn_decode_append(const pa_kv_pool* pool, const void* q, const void* k_new,
+                             const void* v_new, const int32_t* block_tables, int32_t bt_stride,
+                             const int32_t* context_lens, int32_t batch, int32_t num_q_heads,
+                             float scale, int32_t max_context_len, int32_t partition_size,
+                             const int32_t* items, int32_t num_items, void* out, float* partial_out,
+                             float* partial_lse, void* stream) {
+  const char* fn = "paged_attn_decode_append";
+  if (!k_new || !v_new) return fail(PA_EINVAL, "%s: k_new and v_new must be non-NULL", fn);
+  const DecodeArgs a{pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
+                     max_context_len, k_new, v_new};
+  return decode_impl(a, partition_size, out, partial_out, partial_lse, nullptr, 0, false, stream, fn,
+                     items != nullptr, items, num_items);
+}
+
+int paged_attn_decode_cascade_append(const pa_kv_pool* pool, const void* q, const void* k_new,
+                                     const void* v_new, const int32_t* block_tables,
+                                     int32_t bt_stride, const int32_t* context_lens, int32_t batch,
+                                     int32_t num_q_heads, float scale, int32_t max_context_len,
+                                     int32_t partition_size, int32_t prefix_len,
+                                     int32_t prefix_partition_size, const int32_t* group_start,
+                                     int32_t num_groups, int32_t max_group_size, int32_t group_len,
+                                     const int32_t* items, int32_t num_items, float* partial_out,
+                                     float* partial_lse, void* stream) {
+  const char* fn = "paged_attn_decode_cascade_append";
+  if (!k_new || !v_new) return fail(PA_EINVAL, "%s: k_new and v_new must be non-NULL", fn);
+  if (group_len < 0) return fail(PA_EINVAL, "%s: group_len = %d < 0", fn, group_len);
+  return cascade_impl(pool, q, block_tables, bt_stride, context_lens, batch, num_q_heads, scale,
+                      max_context_len, partition_size, prefix_len, prefix_partition_size,
+                      partial_out, partial_lse, stream, fn, items != nullptr, items, num_items,
+                      group_start, group_len > 0 ? num_groups : 0, max_group_size, group_len,
+                      nullptr, 0, false, k_new, v_new);
 }
 
 int paged_attn_decode_scheduled(const pa_kv_pool* pool, const void* q, const int32_t* block_tables,

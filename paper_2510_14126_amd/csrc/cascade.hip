@@ -26,7 +26,7 @@ static_assert(PA_VALU_WAVES == mfma::kWaves, "both halves use the same workgroup
 // than the 3-deep ring of the standalone kernel.
 constexpr int kCascadeValuNbuf = 2;
 
-template <int G, bool TRACE>
+template <int G, bool TRACE, bool APPEND>
 __global__ void __launch_bounds__(64 * mfma::kWaves) __attribute__((amdgpu_waves_per_eu(2, 8)))
 cascade_kernel(const PrefixParams pp, const DecodeParams dp, int prefix_runs, int group_runs,
                int decode_runs) {
@@ -72,9 +72,10 @@ cascade_kernel(const PrefixParams pp, const DecodeParams dp, int prefix_runs, in
   }
   const int wg = idx * hkv + g;
   if constexpr (G == 4) {
-    valu::decode_valu_body<128, 4, PA_VALU_WAVES, kCascadeValuNbuf, TRACE, /*STREAM=*/true>(dp, wg, lds);
+    valu::decode_valu_body<128, 4, PA_VALU_WAVES, kCascadeValuNbuf, TRACE, /*STREAM=*/true, APPEND>(
+        dp, wg, lds);
   } else {
-    mfma::decode_mfma_body<TRACE, /*STREAM=*/true>(dp, wg, lds);
+    mfma::decode_mfma_body<TRACE, /*STREAM=*/true, APPEND>(dp, wg, lds);
   }
 }
 
@@ -97,10 +98,14 @@ hipError_t launch_cascade(const PrefixParams& pp, const DecodeParams& dp, int gr
     hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(64 * mfma::kWaves), 0, stream, pp, dp,
                        (int)prefix_runs, (int)group_runs, (int)decode_runs);
   };
+  // The trace kernels have no fused append.
+  const bool append = dp.k_new != nullptr && !trace;
   if (group == 4)
-    trace ? go(cascade_kernel<4, true>) : go(cascade_kernel<4, false>);
+    trace ? go(cascade_kernel<4, true, false>)
+          : (append ? go(cascade_kernel<4, false, true>) : go(cascade_kernel<4, false, false>));
   else if (group == 8)
-    trace ? go(cascade_kernel<8, true>) : go(cascade_kernel<8, false>);
+    trace ? go(cascade_kernel<8, true, false>)
+          : (append ? go(cascade_kernel<8, false, true>) : go(cascade_kernel<8, false, false>));
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

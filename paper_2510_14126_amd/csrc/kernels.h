@@ -38,6 +38,13 @@ struct DecodeParams {
   int32_t num_items;             // entries of items
   int32_t stream_tiles;          // 1: load the tiles with the streaming cache hint (plain decode)
   float scale_log2;              // softmax scale * log2(e)
+  // Fused KV append (append kernels only): token ctx_b - 1 of every sequence
+  // takes K and V from k_new / v_new [batch][num_kv_heads][D] bf16, and the
+  // work item that holds it writes them into the pools.
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  uint16_t* k_pool_w;            // the same pools as k_pool / v_pool, written
+  uint16_t* v_pool_w;
 };
 
 // Work items (partition, sequence) of a decode grid; one workgroup per item

@@ -460,7 +460,10 @@ constexpr int kLdsBytes = kWaves * 2 * kStageBytes > kMergeLdsBytes ? kWaves * 2
 // STREAM: load the tiles as streaming data (the cascade's per-sequence half,
 // whose tokens come after everything the sequences share and are normally
 // read by this item only).  The hint changes caching, never the results.
-template <bool TRACE, bool STREAM>
+// APPEND: the fused KV append (DecodeParams::k_new): the item that holds
+// token ctx - 1 takes its K and V rows from k_new / v_new in registers
+// (whatever the pool slot holds) and stores them into the slot.
+template <bool TRACE, bool STREAM, bool APPEND = false>
 __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_index, lds_u8_t* smem) {
   const int lane = threadIdx.x & 63;
   const int wave = wave_uniform(threadIdx.x >> 6);
@@ -493,6 +496,28 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
   const int end = min(ctx, start + p.part_tokens);
   const int nblk = end > start ? (end - start + 15) >> 4 : 0;
 
+  // Fused append: block jnew of this item (-1: none) holds the new token in
+  // row rnew; knew / vnew are chunk n (dims 8n .. 8n+7) of its K and V rows.
+  // The lanes of row group rnew % 4 store the rows.
+  int jnew = -1, rnew = 0;
+  uint4 knew = make_uint4(0, 0, 0, 0), vnew = make_uint4(0, 0, 0, 0);
+  if constexpr (APPEND) {
+    if (ctx > 0 && ctx - 1 >= start && ctx - 1 < end) {
+      jnew = ((ctx - 1) >> 4) - j0;
+      rnew = (ctx - 1) & 15;
+      const size_t src = ((size_t)b * p.num_kv_heads + g) * kD + 8 * n;
+      knew = *reinterpret_cast<const uint4*>(p.k_new + src);
+      vnew = *reinterpret_cast<const uint4*>(p.v_new + src);
+      if (wave == 0 && q == (rnew & 3)) {
+        int phys = p.block_tables[(size_t)b * p.bt_stride + ((ctx - 1) >> 4)];
+        phys = min(max(phys, 0), p.num_blocks - 1);
+        const size_t dst = (((size_t)phys * p.num_kv_heads + g) * 16 + rnew) * kD + 8 * n;
+        *reinterpret_cast<uint4*>(p.k_pool_w + dst) = knew;
+        *reinterpret_cast<uint4*>(p.v_pool_w + dst) = vnew;
+      }
+    }
+  }
+
   lds_u8_t* lds = smem;
   lds_u8_t* stages[2] = {lds + (wave * 2) * kStageBytes, lds + (wave * 2 + 1) * kStageBytes};
 
@@ -522,8 +547,17 @@ __device__ __forceinline__ void decode_mfma_body(const DecodeParams& p, int wg_i
       load_chunks<kAux>(T.k, kbase + id * blk_stride, lane_off, bytes);
       load_chunks<kAux>(T.v, vbase + id * blk_stride, lane_off, bytes);
     };
-    auto run = [&](const MfmaTile& T, int i) {
+    auto run = [&](MfmaTile& T, int i) {
       const int valid = min(16, end - (start + (c0 + i) * 16));
+      if constexpr (APPEND) {
+        // the new token's rows replace whatever the slot held (the ring slot
+        // is loaded again before its next use)
+        if (c0 + i == jnew) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (4 * u + q == rnew) { T.k[u] = knew; T.v[u] = vnew; }
+        }
+      }
       lds_u8_t* vb = stages[flip];
       flip ^= 1;
       const int lim[1] = {valid};

@@ -241,8 +241,10 @@ constexpr int valu_lds_bytes() { return (2 * W * G + W * 4 * G * D) * 4; }
 // One work item (partition, sequence, KV head) = workgroup `wg_index`;
 // `smem` points at valu_lds_bytes<D, G, W>() bytes of LDS.  STREAM: load the
 // tiles as streaming data (kLoadStreaming); it changes caching, never the
-// results.
-template <int D, int G, int W, int NBUF, bool TRACE, bool STREAM>
+// results.  APPEND: the fused KV append (DecodeParams::k_new): the item that
+// holds token ctx - 1 takes its K and V rows from k_new / v_new in registers
+// (whatever the pool slot holds) and stores them into the slot.
+template <int D, int G, int W, int NBUF, bool TRACE, bool STREAM, bool APPEND = false>
 __device__ __forceinline__ void decode_valu_body(const DecodeParams& p, int wg_index, lds_u8_t* smem) {
   constexpr int R = G / 4;
   constexpr int DPL = D / 16;
@@ -290,6 +292,35 @@ __device__ __forceinline__ void decode_valu_body(const DecodeParams& p, int wg_i
   const int end = min(n, start + p.part_tokens);
   const int nblk = end > start ? (end - start + 15) >> 4 : 0;
 
+  // Fused append: block jnew of this item (-1: none) holds the new token in
+  // row rnew; knew / vnew are the lane's slice of its K and V rows (dims
+  // (D/16)*tok ..).  The lanes of row group rnew % 4 store the rows.
+  constexpr int VW = D / 32;
+  int jnew = -1, rnew = 0;
+  uint32_t knew[VW], vnew[VW];
+  if constexpr (APPEND) {
+    if (n > 0 && n - 1 >= start && n - 1 < end) {
+      jnew = ((n - 1) >> 4) - j0;
+      rnew = (n - 1) & 15;
+      const size_t src = ((size_t)b * p.num_kv_heads + g) * D + (D / 16) * tok;
+#pragma unroll
+      for (int w = 0; w < VW; ++w) {
+        knew[w] = reinterpret_cast<const uint32_t*>(p.k_new + src)[w];
+        vnew[w] = reinterpret_cast<const uint32_t*>(p.v_new + src)[w];
+      }
+      if (wave == 0 && grp == (rnew & 3)) {
+        int phys = p.block_tables[(size_t)b * p.bt_stride + ((n - 1) >> 4)];
+        phys = min(max(phys, 0), p.num_blocks - 1);
+        const size_t dst = (((size_t)phys * p.num_kv_heads + g) * 16 + rnew) * D + (D / 16) * tok;
+#pragma unroll
+        for (int w = 0; w < VW; ++w) {
+          reinterpret_cast<uint32_t*>(p.k_pool_w + dst)[w] = knew[w];
+          reinterpret_cast<uint32_t*>(p.v_pool_w + dst)[w] = vnew[w];
+        }
+      }
+    }
+  }
+
   WaveState<D, G> S;
 #pragma unroll
   for (int k = 0; k < R; ++k) { S.m[k] = -__builtin_inff(); S.l[k] = 0.f; }
@@ -322,8 +353,20 @@ __device__ __forceinline__ void decode_valu_body(const DecodeParams& p, int wg_i
       load_rows<D, kAux>(T.k, kbase + id * blk_stride, roff, bytes);
       load_rows<D, kAux>(T.v, vbase + id * blk_stride, roff, bytes);
     };
-    auto run = [&](const KvTile<D>& T, int i) {
+    auto run = [&](KvTile<D>& T, int i) {
       const int valid = min(16, end - (start + (c0 + i) * 16));
+      if constexpr (APPEND) {
+        // the new token's rows replace whatever the slot held (the ring slot
+        // is loaded again before its next use)
+        if (c0 + i == jnew) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (4 * u + grp == rnew) {
+#pragma unroll
+              for (int w = 0; w < VW; ++w) { T.k[u][w] = knew[w]; T.v[u][w] = vnew[w]; }
+            }
+        }
+      }
       if (valid == 16)
         process_tile<D, G, false>(S, T, qv, 16, grp, tok, p.scale_log2);
       else

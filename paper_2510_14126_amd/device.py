@@ -138,6 +138,34 @@ class PagedBatch:
                                   self.out if out is None else out, self.part_o, self.part_lse,
                                   stream)
 
+    def append(self, k_new, v_new, stream=None, pool=None) -> None:
+        """Write the new token's K and V rows (device bf16 [batch][Hkv][D])
+        at position ctx - 1 of every sequence (``paged_attn_append_kv``)."""
+        binding.paged_attn_append_kv(self.pool if pool is None else pool, k_new, v_new, self.bt,
+                                     self.bt_stride, self.ctx, self.batch, stream)
+
+    def decode_append(self, k_new, v_new, stream=None, out=None, pool=None, q=None) -> None:
+        """``append`` and ``decode`` in one launch, in the same launch
+        configuration as ``decode`` (work list, cascade, groups)."""
+        pool = self.pool if pool is None else pool
+        q = self.q if q is None else q
+        n = 0 if self.items is None else int(self.items.numel())
+        items = self.items if n else None
+        if self.prefix_len or self.group_len:
+            g = self.group_len > 0
+            binding.paged_attn_decode_cascade_append(
+                pool, q, k_new, v_new, self.bt, self.bt_stride, self.ctx, self.batch, self.hq,
+                self.w.scale, self.max_ctx, self.partition_size, self.prefix_len,
+                self.prefix_partition_size, self.group_start if g else None,
+                self.num_groups if g else 0, self.max_group_size if g else 0, self.group_len, items,
+                n, self.part_o, self.part_lse, stream)
+            return
+        binding.paged_attn_decode_append(pool, q, k_new, v_new, self.bt, self.bt_stride, self.ctx,
+                                         self.batch, self.hq, self.w.scale, self.max_ctx,
+                                         self.partition_size, items, n,
+                                         self.out if out is None else out, self.part_o,
+                                         self.part_lse, stream)
+
     def reduce(self, stream=None, out=None) -> None:
         if self.group_len:
             binding.paged_attn_reduce_cascade_groups(

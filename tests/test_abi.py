@@ -27,7 +27,7 @@ def declared_functions():
 
 def test_header_and_library_agree():
     names = declared_functions()
-    assert len(names) == 35, names
+    assert len(names) == 37, names
     lib = pa.library()
     for n in names:
         assert hasattr(lib, n), f"library does not export {n}"
@@ -189,6 +189,37 @@ def test_decode_validation(over, code):
     p = make_pool()
     with pytest.raises(pa.PagedAttnError) as e:
         _decode(p, **over)
+    assert e.value.code == code, pa.pa_last_error()
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(k_new=None), pa.PA_EINVAL),
+    (dict(v_new=None), pa.PA_EINVAL),
+    (dict(k_new=0x5008), pa.PA_EINVAL),                # misaligned
+    (dict(v_new=0x6004), pa.PA_EINVAL),
+    (dict(num_q_heads=24), pa.PA_EUNSUPPORTED),
+    (dict(items=0x7000, num_items=-1), pa.PA_EINVAL),
+])
+def test_fused_append_validation(over, code):
+    """Argument checks of the fused append + decode entry points, before any
+    HIP call (fake device addresses)."""
+    p = make_pool()
+    args = dict(q=0x1000, k_new=0x5000, v_new=0x6000, block_tables=0x2000, bt_stride=4,
+                context_lens=0x3000, batch=2, num_q_heads=32, scale=0.088, max_context_len=64,
+                partition_size=0, items=None, num_items=0, out=0x4000, partial_out=None,
+                partial_lse=None)
+    args.update(over)
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.paged_attn_decode_append(p, **args)
+    assert e.value.code == code, pa.pa_last_error()
+    cargs = dict(q=0x1000, k_new=0x5000, v_new=0x6000, block_tables=0x2000, bt_stride=4,
+                 context_lens=0x3000, batch=2, num_q_heads=32, scale=0.088, max_context_len=64,
+                 partition_size=32, prefix_len=16, prefix_partition_size=16, group_start=None,
+                 num_groups=0, max_group_size=0, group_len=0, items=None, num_items=0,
+                 partial_out=0x8000, partial_lse=0x9000)
+    cargs.update({k: v for k, v in over.items() if k in cargs})
+    with pytest.raises(pa.PagedAttnError) as e:
+        pa.paged_attn_decode_cascade_append(p, **cargs)
     assert e.value.code == code, pa.pa_last_error()
 
 
