@@ -925,6 +925,37 @@ def measure(k, w, args, cpu, copy_gbps, headline, with_extend):
                    "gbps": round(app_bytes / (app_ms * 1e-3) / 1e9, 2),
                    "note": "one launch per step; launch-latency bound at these sizes"}
 
+    # A serving loop's decode iteration: append, decode and reduce as three
+    # launches, against the fused append + decode and the reduce (the same
+    # rows as above, so the pools stay unchanged).
+    def iteration(i, fused):
+        pool, q = reps[i % R]
+        if fused:
+            base.decode_append(k_new, v_new, sh, pool=pool, q=q)
+        else:
+            binding.paged_attn_append_kv(pool, k_new, v_new, base.bt, base.bt_stride, base.ctx,
+                                         base.batch, sh)
+            base.decode(sh, pool=pool, q=q)
+        if split:
+            reduce()
+
+    iter_us = {}
+    for fused in (False, True):
+        for i in range(3):
+            iteration(i, fused)
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for i in range(K):
+            iteration(i, fused)
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        iter_us["fused" if fused else "append_then_decode"] = round(
+            1e3 * ev[0].elapsed_time(ev[1]) / K, 3)
+    iteration_line = {"append_then_decode_us": iter_us["append_then_decode"],
+                      "fused_append_decode_us": iter_us["fused"],
+                      "note": "append + decode (+ reduce) per step as separate launches, and with "
+                              "paged_attn_decode(_cascade)_append; same replicas as the main loop"}
+
     extend_line = run_extend(w, base, reps, R, K, stream, sh, binding) if with_extend else None
 
     # parity spot check of the benchmarked launch configuration
@@ -984,6 +1015,7 @@ def measure(k, w, args, cpu, copy_gbps, headline, with_extend):
                      "bytes_per_launch": int(alg_bytes)},
         "gather_reference": gather_line,
         "append_kv": append_line,
+        "decode_iteration": iteration_line,
         "cpu_baseline": cpu,
     }
     if extend_line is not None:
