@@ -176,6 +176,20 @@ static void validation() {
   CHECK(paged_attn_decode_cascade_trace(p, q, bt, 160, ctx, 10, 32, 0.1f, 2300, 512, 2048, 512,
                                         nullptr, 0, 0, 0, nullptr, 0, po, pl, trace.data(), lay[6],
                                         nullptr) == PA_EHIP);
+  void* kn = reinterpret_cast<void*>(0x90000);
+  void* vn = reinterpret_cast<void*>(0xa0000);
+  CHECK(paged_attn_decode_append(p, q, nullptr, vn, bt, 8, ctx, 2, 32, 0.1f, 128, 64, nullptr, 0,
+                                 out, po, pl, nullptr) == PA_EINVAL);   // k_new missing
+  CHECK(paged_attn_decode_append(p, q, reinterpret_cast<char*>(kn) + 8, vn, bt, 8, ctx, 2, 32, 0.1f,
+                                 128, 64, nullptr, 0, out, po, pl, nullptr) == PA_EINVAL);  // misaligned
+  CHECK(paged_attn_decode_append(p, q, kn, vn, bt, 8, ctx, 2, 32, 0.1f, 128, 64, nullptr, 0, out, po,
+                                 pl, nullptr) == PA_EHIP);
+  CHECK(paged_attn_decode_cascade_append(p, q, kn, vn, bt, 160, ctx, 10, 32, 0.1f, 2300, 512, 2048,
+                                         512, nullptr, 0, 0, -1, nullptr, 0, po, pl, nullptr) ==
+        PA_EINVAL);                                                   // negative group_len
+  CHECK(paged_attn_decode_cascade_append(p, q, kn, vn, bt, 160, ctx, 10, 32, 0.1f, 2300, 512, 2048,
+                                         512, nullptr, 0, 0, 0, nullptr, 0, po, pl, nullptr) ==
+        PA_EHIP);
   CHECK(paged_attn_reduce(po, pl, ctx, 2, 32, 128, 0, 4, out, nullptr) == PA_EINVAL);
   CHECK(paged_attn_extend(p, q, ctx, 10, bt, 600, ctx, 2, 32, 0.1f, 9000, 10, out, nullptr) ==
         PA_EUNSUPPORTED);
