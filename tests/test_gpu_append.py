@@ -98,19 +98,21 @@ def test_append_out_of_range_ids_stay_inside_the_pool():
     pool.close()
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["append-then-decode", "fused"])
 @pytest.mark.parametrize("hq,hkv,d,S", [(32, 8, 128, 64), (64, 8, 128, 0), (8, 2, 64, 32)],
                          ids=["g4-d128-split", "g8-d128", "g4-d64-split"])
-def test_decode_loop_append_then_attend(hq, hkv, d, S):
+def test_decode_loop_append_then_attend(hq, hkv, d, S, fused):
     """Prompts of several lengths grow token by token: a fresh block comes
     from the pool allocator whenever a token starts one, the step's K/V is
-    appended on the GPU, and the step's attention must match the oracle run
-    on the oracle-appended pools; the pools stay bit-identical throughout."""
+    appended on the GPU (by the append kernel, or inside the decode launch
+    when fused), and the step's attention must match the oracle run on the
+    oracle-appended pools; the pools stay bit-identical throughout."""
     from paper_2510_14126_amd import binding
     from paper_2510_14126_amd.device import PagedBatch
     steps = 40
     prompts = [1, 15, 16, 17, 100, 255]
     B = len(prompts)
-    say(f"decode loop hq={hq} hkv={hkv} d={d} S={S} prompts={prompts} steps={steps}")
+    say(f"decode loop hq={hq} hkv={hkv} d={d} S={S} fused={fused} prompts={prompts} steps={steps}")
     case = logical_case(101, B, hq, hkv, d, prompts)
     growth = sum((p + steps + 15) // 16 - (p + 15) // 16 for p in prompts)
     w = page_case(case, 102, share_prefix=False, extra_blocks=growth + 3,
@@ -131,11 +133,17 @@ def test_decode_loop_append_then_attend(hq, hkv, d, S):
                 bt[b, t // 16] = binding.kv_pool_alloc(alloc, 1)[0]
         kn, vn, q = _bf16(rng, (B, hkv, d)), _bf16(rng, (B, hkv, d)), _bf16(rng, (B, hq, d))
         bt_dev, ctx_dev = _dev(bt), _dev(ctx)
-        binding.paged_attn_append_kv(alloc, _dev(kn), _dev(vn), bt_dev, W, ctx_dev, B)
+        if not fused:
+            binding.paged_attn_append_kv(alloc, _dev(kn), _dev(vn), bt_dev, W, ctx_dev, B)
         kp, vp = append_kv(kp, vp, bt, ctx, kn, vn)
         ws = replace(w, context_lens=ctx.copy(), block_tables=bt.copy(), q=q, k_pool=kp, v_pool=vp)
         pb = PagedBatch(ws, DEV, partition_size=S, register_blocks=False, k_pool=k_dev, v_pool=v_dev)
-        pb.run()
+        if fused:
+            pb.decode_append(_dev(kn), _dev(vn))
+            if pb.needs_reduce:
+                pb.reduce()
+        else:
+            pb.run()
         torch.cuda.synchronize()
         out = pb.out_bits()
         pb.close()
